@@ -1,0 +1,45 @@
+"""Runs the oracle pins against one build of oracle.c (used by
+test_oracle_mutations in a child process).  Exit 0: every pin passed;
+exit 3: some pin failed."""
+import os
+import sys
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+import gen  # noqa: E402
+import oracle  # noqa: E402
+import test_oracle_invariants as inv  # noqa: E402
+import test_oracle_pins as pins  # noqa: E402
+
+
+def main(lib_path, bf_exe):
+    oracle.use_library(lib_path)
+    orc = oracle
+    checks = [
+        lambda: [pins.test_worked_example_plan(orc, n) for n in
+                 ("W0_single_hot_expert.json", "W1_nonmonotone_bisection.json",
+                  "W2_proportional_split.json", "W4_two_slots_dispatch_pack.json",
+                  "W5_visit_order.json")],
+        lambda: pins.test_w6_pack_order(orc),
+        lambda: pins.test_w1_feasibility_is_not_monotone(orc),
+        lambda: pins.test_w3_rounding_keeps_both_margins(orc),
+        lambda: pins.test_w4_dispatch_and_pack(orc),
+        lambda: pins.test_apportion_matches_closest_vector_search(orc),
+        lambda: pins.test_s1_no_slots_is_stable_counting_sort(orc),
+        lambda: pins.test_s2_balanced_load_needs_no_probe(orc),
+        lambda: [pins.test_s3_single_hot_expert_closed_form(orc, R) for R in (2, 5)],
+        lambda: pins.test_bruteforce_small_random_groups(orc, bf_exe),
+        lambda: [inv.test_fuzz_case(orc, s) for s in range(40)],
+    ]
+    for i, chk in enumerate(checks):
+        try:
+            chk()
+        except Exception as ex:  # a failed pin
+            print(f"caught by check {i}: {type(ex).__name__}: {str(ex)[:120]}")
+            return 3
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv[1], sys.argv[2]))

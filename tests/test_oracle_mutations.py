@@ -1,0 +1,89 @@
+"""Mutation check of the oracle's pins: plant one plausible mistake at a time
+in a copy of oracle/oracle.c (a flipped tie-break, a dropped term, a floor for
+a ceiling, a skipped pass, a wrong index), build it, and require that at
+least one pin or invariant check fails.  Runs on the CPU only."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                   "oracle", "oracle.c")
+
+MUTATIONS = {
+    "argmax_tie_to_higher_rank": ("if (best < 0 || slk[t] > slk[best]) best = t;",
+                                  "if (best < 0 || slk[t] >= slk[best]) best = t;"),
+    "delta_ignores_cap": ("int64_t delta = min64(min64(exc[r], slk[best]), cap);",
+                          "int64_t delta = min64(exc[r], slk[best]);"),
+    "u_min_inclusive": ("if (delta < g->u_min) break;",
+                        "if (delta <= g->u_min) break;"),
+    "mid_rounds_up": ("int64_t tau = (lo + hi) / 2;",
+                      "int64_t tau = (lo + hi + 1) / 2;"),
+    "tau_lo_floor": ("*lo = (g->beta_num * m + g->beta_den - 1) / g->beta_den;",
+                     "*lo = g->beta_num * m / g->beta_den;"),
+    "mean_floor": ("int64_t m = (c->L + g->R - 1) / g->R;",
+                   "int64_t m = c->L / g->R;"),
+    "no_locality": ("int64_t q = locality ? min64(lamhat[t], u) : 0;",
+                    "int64_t q = 0;"),
+    "remainder_tie_to_later_host": (
+        "if (!taken[i] && (best < 0 || rem[i] > rem[best])) best = i;",
+        "if (!taken[i] && (best < 0 || rem[i] >= rem[best])) best = i;"),
+    "order_ascending": ("if (x->key != y->key) return x->key > y->key ? -1 : 1;",
+                        "if (x->key != y->key) return x->key < y->key ? -1 : 1;"),
+    "order_ties_to_higher_id": ("return x->id < y->id ? -1 : (x->id > y->id);",
+                                "return x->id > y->id ? -1 : (x->id < y->id);"),
+    "replica_pslot_without_main_offset": ("host_pslot[j] = nm + s;",
+                                          "host_pslot[j] = s;"),
+    "lookup_inclusive": ("if (j < C + qi) {", "if (j <= C + qi) {"),
+    "pack_slot_major": (
+        "  for (int32_t t = 0; t < R; t++)\n    for (int32_t s = 0; s < NS; s++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e >= 0 && home(g, e) == rank) {\n        memcpy",
+        "  for (int32_t s = 0; s < NS; s++)\n    for (int32_t t = 0; t < R; t++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e >= 0 && home(g, e) == rank) {\n        memcpy"),
+    "proportional_split_on_full_quota": ("uhat[i] = u - q; /* residual quota */",
+                                         "uhat[i] = u; /* residual quota */"),
+    "residual_not_updated": ("        uhat[i] -= qv[i];\n", "\n"),
+    "home_keeps_nothing_back": ("Ut[(int64_t)e * R + home(g, e)] -= delta;",
+                                "Ut[(int64_t)e * R + home(g, e)] -= 0;"),
+}
+
+
+RUNNER = os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                      "mutation_runner.py")
+
+
+@pytest.fixture(scope="module")
+def bruteforce(tmp_path_factory):
+    return pins.build_bruteforce(tmp_path_factory.mktemp("bfm"))
+
+
+def _run(lib_path, bf, timeout=120):
+    """Exit code of the pin harness on one build; a hang counts as a failure
+    (returned as 124)."""
+    try:
+        return subprocess.run([sys.executable, RUNNER, lib_path, bf],
+                              capture_output=True, text=True,
+                              timeout=timeout).returncode
+    except subprocess.TimeoutExpired:
+        return 124
+
+
+def test_unmutated_oracle_passes_the_harness(orc, bruteforce):
+    assert _run(orc._LIB, bruteforce) == 0
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_is_caught(bruteforce, tmp_path, name):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique/found: {name}"
+    mdir = tmp_path / name
+    mdir.mkdir()
+    (mdir / "oracle.c").write_text(src.replace(old, new))
+    (mdir / "oracle.h").write_text(open(SRC[:-2] + ".h").read())
+    so = str(mdir / "libmut.so")
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-o", so,
+                    str(mdir / "oracle.c")], check=True)
+    # exit 3: a pin failed; a crash or a hang is also a detection
+    assert _run(so, bruteforce, timeout=30) != 0, f"no pin detects {name}"

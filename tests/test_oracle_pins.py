@@ -1,0 +1,267 @@
+"""Pins of the oracle against what the paper and the mathematics fix:
+hand-derived worked examples (tests/golden), closed forms, special cases that
+reduce to library routines, a brute-force optimum bound and an independent
+characterisation of the rounding step.  No GPU needed."""
+import glob
+import itertools
+import json
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+from invariants import check_dispatch, check_pack, check_plan
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def load_golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def group_of(orc, d):
+    return orc.Group(**d["group"])
+
+
+# ---------------------------------------------------------------- W0..W4
+
+@pytest.mark.parametrize("name", ["W0_single_hot_expert.json",
+                                  "W1_nonmonotone_bisection.json",
+                                  "W2_proportional_split.json",
+                                  "W4_two_slots_dispatch_pack.json",
+                                  "W5_visit_order.json"])
+def test_worked_example_plan(orc, name):
+    d = load_golden(name)
+    g = group_of(orc, d)
+    load = np.array(d["load"], np.int32)
+    assert orc.bisect_trace(load, g) == [tuple(x) for x in d["trace"]]
+    p = orc.plan(load, g)
+    assert p.status == 0
+    assert p.tau_star == d["tau_star"]
+    if "tau_lo0" in d:
+        assert (p.stats[1], p.stats[2]) == (d["tau_lo0"], d["tau_hi0"])
+    assert p.stats[3] == len(d["trace"])
+    assert p.slot_expert.tolist() == d["slot_expert"]
+    if "quota" in d:
+        assert p.quota.tolist() == d["quota"]
+    if "quota_nonzero" in d:
+        exp = np.zeros_like(p.quota)
+        for key, v in d["quota_nonzero"].items():
+            e, t = map(int, key.split(","))
+            exp[e, t] = v
+        assert np.array_equal(p.quota, exp)
+    csr = d.get("reroute_csr", d)
+    for f in ("host_ptr", "host_rank", "host_pslot"):
+        if f in csr:
+            assert getattr(p, f).tolist() == csr[f], f
+    if "reroute" in d:
+        assert p.reroute.tolist() == d["reroute"]
+    check_plan(load, g, p)
+
+
+def test_w1_feasibility_is_not_monotone(orc):
+    d = load_golden("W1_nonmonotone_bisection.json")
+    g = group_of(orc, d)
+    load = np.array(d["load"], np.int32)
+    lo, hi = d["probe_range"]
+    feas = [t for t in range(lo, hi + 1) if orc.probe(load, g, t)[0]]
+    assert feas == [t for t in d["feasible_taus"] if lo <= t <= hi]
+
+
+def test_w3_rounding_keeps_both_margins(orc):
+    d = load_golden("W3_rounding_margins.json")
+    for step in d["steps"]:
+        assert orc.apportion(step["demand"], step["ures"]).tolist() == step["out"]
+
+
+def test_w4_dispatch_and_pack(orc):
+    d = load_golden("W4_two_slots_dispatch_pack.json")
+    g = group_of(orc, d)
+    load = np.array(d["load"], np.int32)
+    p = orc.plan(load, g)
+    topk = np.array(d["topk"], np.int32)
+    T, k = topk.shape
+    # token rows that identify their token
+    x = (np.arange(T)[:, None] * 100 + np.arange(4)[None, :]).astype(np.uint16)
+    counts, st = orc.count(topk, g.E)
+    assert st == 0 and counts[0].tolist() == d["load"][d["dispatch_rank"]]
+    send, ros, boff, st = orc.dispatch(x, topk, d["dispatch_rank"], g, p)
+    assert st == 0
+    assert boff.tolist() == d["block_off"]
+    assert ros.tolist() == d["row_of_slot"]
+    assert [int(r[0]) // 100 for r in send] == d["send_token_of_row"]
+    check_dispatch(x, topk, d["dispatch_rank"], g, p, send, ros, boff)
+    w = np.arange(g.n_main * 6, dtype=np.uint16).reshape(g.n_main, 6)
+    staging, doff, n_out, st = orc.pack(w, d["pack_rank"], g, p, cap=4)
+    assert st == 0 and n_out == len(d["pack_experts"])
+    assert doff.tolist() == d["dest_off"]
+    for n, e in enumerate(d["pack_experts"]):
+        assert np.array_equal(staging[n], w[e])
+    check_pack(w, d["pack_rank"], g, p, staging, doff, n_out)
+
+
+def test_w6_pack_order(orc):
+    d = load_golden("W6_pack_order.json")
+    g = group_of(orc, d)
+    X = np.array(d["slot_expert"], np.int32)
+    p = orc.Plan(X, None, None, None, None, None, None, 0)
+    w = (np.arange(g.n_main)[:, None] * 1000 + np.arange(5)[None, :]).astype(np.uint16)
+    for case in d["cases"]:
+        r = case["rank"]
+        wr = w + np.uint16(100 * r)
+        staging, doff, n_out, st = orc.pack(wr, r, g, p, cap=8)
+        assert st == 0 and doff.tolist() == case["dest_off"]
+        assert n_out == len(case["experts"])
+        for n, e in enumerate(case["experts"]):
+            assert np.array_equal(staging[n], wr[e - r * g.n_main])
+
+
+# ---------------------------------------------------------------- rounding
+
+def _hamilton_by_search(demand, ures):
+    """Independent characterisation: the largest-remainder result is the
+    integer vector q (0 <= q_i <= u_i, sum q = demand) closest to the exact
+    shares demand*u_i/D in squared distance; among equally close vectors the
+    earlier host receives the extra unit (lexicographically largest q)."""
+    D = sum(ures)
+    best = None
+    for q in itertools.product(*[range(u + 1) for u in ures]):
+        if sum(q) != demand:
+            continue
+        cost = sum((D * qi - demand * ui) ** 2 for qi, ui in zip(q, ures))
+        key = (cost, tuple(-v for v in q))
+        if best is None or key < best[0]:
+            best = (key, q)
+    return list(best[1])
+
+
+def test_apportion_matches_closest_vector_search(orc):
+    rng = np.random.default_rng(7)
+    for _ in range(400):
+        nh = int(rng.integers(1, 5))
+        ures = [int(v) for v in rng.integers(0, 7, nh)]
+        if sum(ures) == 0:
+            continue
+        demand = int(rng.integers(0, sum(ures) + 1))
+        assert orc.apportion(demand, ures).tolist() == \
+            _hamilton_by_search(demand, ures), (demand, ures)
+
+
+# ---------------------------------------------------------------- special cases
+
+def test_s1_no_slots_is_stable_counting_sort(orc):
+    """With no redundant slots the plan is the identity and the dispatch
+    permutation is a stable sort of the routed slots by expert id."""
+    rng = np.random.default_rng(3)
+    for R, nm, T, k in [(4, 4, 300, 3), (2, 8, 129, 2), (8, 1, 64, 1)]:
+        g = orc.Group(R, R * nm, 0, 1)
+        topk_all = rng.integers(-1, g.E, (R, T, k)).astype(np.int32)
+        load, _ = orc.count(topk_all, g.E, R)
+        p = orc.plan(load, g)
+        assert p.stats[4] == 0
+        assert np.array_equal(p.quota.sum(1), load.sum(0))
+        for r in (0, R - 1):
+            x = rng.integers(0, 2 ** 16, (T, 16)).astype(np.uint16)
+            send, ros, boff, st = orc.dispatch(x, topk_all[r], r, g, p)
+            assert st == 0
+            flat = topk_all[r].reshape(-1)
+            valid = np.nonzero(flat >= 0)[0]
+            order = valid[np.argsort(flat[valid], kind="stable")]
+            exp_rows = np.full(flat.size, -1)
+            exp_rows[order] = np.arange(order.size)
+            assert np.array_equal(ros, exp_rows)
+            assert np.array_equal(send[: order.size], x[order // k])
+
+
+def test_s2_balanced_load_needs_no_probe(orc):
+    for R, nm in [(4, 2), (8, 4), (64, 4)]:
+        g = orc.Group(R, R * nm, 2, 1024)
+        load = np.full((R, R * nm), 40, np.int32)
+        p = orc.plan(load, g)
+        assert p.stats[3] == 0 and p.stats[4] == 0
+        assert p.tau_star == p.stats[2] == 40 * R * nm
+        assert (p.slot_expert == -1).all()
+
+
+@pytest.mark.parametrize("R", [2, 3, 5, 8, 16])
+def test_s3_single_hot_expert_closed_form(orc, R):
+    """All load L on expert 0 of rank 0, u_min = 1: every threshold from the
+    mean up is feasible, so tau* = tau_lo0, and the replicas fill ranks
+    1, 2, ... with tau* each, the last one taking the remainder."""
+    rng = np.random.default_rng(R)
+    for beta in [(101, 100), (100, 100), (5, 4)]:
+        for L in rng.integers(R * 3, 5000, 4):
+            L = int(L)
+            g = orc.Group(R, R, 1, 1, *beta)
+            load = np.zeros((R, R), np.int32)
+            load[int(rng.integers(0, R)), 0] = L
+            m = -(-L // R)
+            tau_lo = -(-beta[0] * m // beta[1])
+            p = orc.plan(load, g)
+            if tau_lo >= L:
+                assert p.stats[4] == 0
+                continue
+            tau = tau_lo
+            assert p.tau_star == tau
+            n_rep = -(-(L - tau) // tau)
+            exp = [tau] * n_rep
+            exp[-1] = L - tau - tau * (n_rep - 1)
+            assert p.quota[0, 0] == tau
+            assert p.quota[0, 1:1 + n_rep].tolist() == exp
+            assert (p.quota[0, 1 + n_rep:] == 0).all()
+
+
+# ---------------------------------------------------------------- brute force
+
+def build_bruteforce(outdir):
+    src = os.path.join(os.path.dirname(__file__), "native", "bruteforce.c")
+    exe = os.path.join(str(outdir), "bruteforce")
+    subprocess.run(["gcc", "-O2", "-o", exe, src], check=True)
+    return exe
+
+
+@pytest.fixture(scope="module")
+def bruteforce(tmp_path_factory):
+    return build_bruteforce(tmp_path_factory.mktemp("bf"))
+
+
+def _bf(exe, R, E, NS, lam):
+    out = subprocess.run([exe, str(R), str(E), str(NS)] + [str(int(v)) for v in lam],
+                         check=True, capture_output=True, text=True)
+    return int(out.stdout)
+
+
+def test_s4_bruteforce_bounds_tiny_config(orc, gen_mod, bruteforce):
+    """Tiny workload (R=4, E=16, 2 slots), u_min = 1: the true optimum of
+    the max rank load over every full placement never exceeds the planner's
+    realised max load, which never exceeds tau*."""
+    c = gen_mod.config(1)
+    ratios = []
+    for m in range(3):
+        tk = gen_mod.topk_all(c, m)
+        load, _ = orc.count(tk, c.E, c.R)
+        g = orc.Group(c.R, c.E, c.n_slot, 1)
+        p = orc.plan(load, g)
+        after = p.quota.sum(0).max()
+        opt = _bf(bruteforce, c.R, c.E, c.n_slot, load.sum(0))
+        assert opt <= after <= p.tau_star
+        ratios.append(after / opt)
+    assert max(ratios) < 1.2
+
+
+def test_bruteforce_small_random_groups(orc, bruteforce):
+    rng = np.random.default_rng(11)
+    for _ in range(30):
+        R = int(rng.integers(2, 5))
+        nm = int(rng.integers(1, 3))
+        NS = int(rng.integers(1, 3))
+        g = orc.Group(R, R * nm, NS, 1)
+        lam = (rng.pareto(1.2, g.E) * 20).astype(np.int32) + 1
+        load = np.zeros((R, g.E), np.int32)
+        load[0] = lam
+        p = orc.plan(load, g)
+        opt = _bf(bruteforce, R, g.E, NS, lam)
+        after = p.quota.sum(0).max()
+        assert opt <= after <= p.tau_star
