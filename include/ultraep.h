@@ -1,0 +1,199 @@
+/*
+ * ultraep.h — C ABI of the MI355X (gfx950) library for UltraEP's
+ * per-microbatch, per-layer balancing path (arXiv 2606.04101):
+ *
+ *   1. ultraep_count          exact per-expert loads from top-k routing ids
+ *   2. ultraep_plan           quota-driven replication (SolveReplication) and
+ *                             reroute split (SolveReroute), Algorithm 1
+ *   3. ultraep_dispatch       token-to-replica assignment and bf16 row scatter
+ *                             into per-destination, per-replica blocks
+ *   4. ultraep_pack_replicas  local half of weight distribution: the blobs of
+ *                             this rank's replicated main experts copied into
+ *                             per-destination staging
+ *
+ * Conventions for every call:
+ *   - Buffer pointers are DEVICE pointers unless marked "host".  The caller
+ *     owns and allocates every buffer; the library never allocates, never
+ *     frees, never synchronises the host, keeps no state between calls and
+ *     issues no memset, so every call can be captured into a HIP graph.
+ *   - Work is enqueued on `stream` in order; results are ready when the
+ *     stream reaches that point.  Calls on different streams must use
+ *     distinct output and workspace buffers.
+ *   - Return value: ULTRAEP_OK, or ULTRAEP_EINVAL for an argument problem
+ *     that the host can see (nothing is launched), or ULTRAEP_EDEVICE when a
+ *     launch fails.
+ *   - Problems visible only in device data are reported through a device
+ *     status word: the first failing kernel stores its (negative) code into
+ *     *status if it still holds 0.  The caller zeroes the word before a
+ *     sequence of calls and reads it after its own synchronisation.  When
+ *     the status is nonzero the outputs of the failing call are undefined.
+ *   - Layouts are row-major.  With n_main = E / R main experts per rank,
+ *     home rank h(e) = e / n_main (main experts in contiguous blocks),
+ *     S = n_main + n_slot physical slots per rank (slot p < n_main is main
+ *     expert r*n_main + p, slot n_main + s is redundant slot s) and
+ *     ncol = E + R * n_slot CSR entries at most.
+ *   - bf16 data are moved as raw 16-bit patterns (never converted).
+ *
+ * Supported sizes (else ULTRAEP_EINVAL): 1 <= R <= 64, E % R == 0,
+ * E <= 1024, 0 <= n_slot, R * n_slot <= 256, u_min >= 1,
+ * 1 <= beta_den <= beta_num <= 2^20, 1 <= k <= min(E, 64), T >= 0,
+ * T * k < 2^31, H % 8 == 0, W % 8 == 0, 16-byte aligned x / send / w_main /
+ * staging.  The total load of a plan must not exceed 2^30 tokens (device
+ * status ULTRAEP_EDATA otherwise).
+ */
+#ifndef ULTRAEP_H
+#define ULTRAEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  ULTRAEP_OK = 0,
+  ULTRAEP_EINVAL = -1,  /* bad argument (host-visible); nothing launched */
+  ULTRAEP_ENOSPC = -2,  /* device: staging capacity too small */
+  ULTRAEP_EDEVICE = -3, /* a kernel launch failed */
+  ULTRAEP_EDATA = -4    /* device: ids out of range, negative or oversized
+                           loads, or a load row that disagrees with topk */
+};
+
+/* EP group metadata and the planner's constants (host struct).
+ * Table 1 of the paper: R ranks, E logical experts, N_slot redundant slots per
+ * rank, quota floor u_min (1024 in the paper) and balancing target
+ * beta = beta_num / beta_den (1.01 in the paper, i.e. 101/100). */
+typedef struct {
+  int32_t R;
+  int32_t E;
+  int32_t n_slot;
+  int64_t u_min;
+  int32_t beta_num;
+  int32_t beta_den;
+} ultraep_group;
+
+/* Plan outputs (device buffers; element counts from ultraep_plan_sizes).
+ *   slot_expert [R * n_slot]   X (Table 1): x_{t,s} = expert hosted by
+ *                              redundant slot s of rank t, -1 when empty;
+ *                              slots fill in the order replicas are accepted.
+ *   quota       [E * R]        U (Table 1): u_{e,t} at e * R + t.
+ *   host_ptr    [E + 1]        CSR row pointers over the hosts H(e).
+ *   host_rank   [ncol]         H(e) in order: home first, then replica ranks
+ *                              ascending; -1 padding after host_ptr[E].
+ *   host_pslot  [ncol]         physical slot of that instance on its rank;
+ *                              -1 padding.
+ *   reroute     [R * ncol]     Q (Table 1): q_{r,e,t} at r * ncol + j where j
+ *                              is the CSR entry of (e, t); 0 padding.
+ *   stats       [8] int64      tau*, tau_lo0, tau_hi0, number of bisection
+ *                              probes, number of replicas, max |H(e)|,
+ *                              status (0 or ULTRAEP_EDATA), total load L. */
+typedef struct {
+  int32_t *slot_expert;
+  int32_t *quota;
+  int32_t *host_ptr;
+  int32_t *host_rank;
+  int32_t *host_pslot;
+  int32_t *reroute;
+  int64_t *stats;
+} ultraep_plan_buf;
+
+/* Host only.  Element counts of the seven plan buffers, in struct order, for
+ * group *g (host pointer).  Returns ULTRAEP_EINVAL for an unsupported group. */
+int ultraep_plan_sizes(const ultraep_group *g, size_t counts_out[7]);
+
+/* Step 1 — exact load acquisition (Sec. 4.2 forward pipeline; lambda_{r,e} of
+ * Table 1): counts[b * E + e] = number of (token, k) slots of block b routed
+ * to expert e, for n_groups blocks of T * k ids stored back to back in topk
+ * ([n_groups][T][k] int32).  Id -1 means "not routed" and is skipped; ids
+ * outside [-1, E) are skipped and raise ULTRAEP_EDATA in *status.  One count
+ * per routed slot (no per-token deduplication).  counts is fully written. */
+int ultraep_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
+                  int32_t n_groups, int32_t *counts, int32_t *status,
+                  hipStream_t stream);
+
+/* Step 2 — Algorithm 1 on the load matrix (device, [R][E] int32, row r =
+ * lambda_{r,.}).  SolveReplication binary-searches the integer threshold tau
+ * from tau_lo = ceil(beta * ceil(L / R)) to tau_hi = max_r ell_r with
+ * tau = floor((lo + hi) / 2), running the greedy probe of Sec. 5.1 at each
+ * step (overloaded ranks by descending excess, their main experts by
+ * descending load, transfers of min(excess, slack, remaining load) to the
+ * admissible rank of largest slack, a transfer below u_min ends the expert;
+ * all ties go to the lower id).  The last feasible probe gives X and U; with
+ * no feasible probe every expert stays on its home.  SolveReroute (Sec. 5.2)
+ * lets each host's own tokens consume its quota first, then splits every
+ * source's residual demand over the residual quotas in proportion, sources
+ * in ascending rank order, by largest remainder against the quotas still
+ * unconsumed (ties to the earlier host), which keeps both margins of Q
+ * exact.  Every output buffer is fully written (padding included).  Data
+ * errors (negative loads, L > 2^30) set stats[6] = ULTRAEP_EDATA. */
+int ultraep_plan(const int32_t *load, const ultraep_group *g,
+                 const ultraep_plan_buf *out, hipStream_t stream);
+
+/* Bytes of device workspace ultraep_dispatch / ultraep_dispatch_layout need
+ * (host only; 0 for unsupported arguments). */
+size_t ultraep_dispatch_ws_bytes(int64_t T, int32_t k, const ultraep_group *g);
+
+/* Step 3 — token assignment and dispatch permutation of source rank `rank`
+ * (Sec. 5.2 Token Assignment).  The j-th local slot routed to expert e
+ * (counted over the (token, k) slots in token-major order) goes to the first
+ * instance of H(e) whose cumulative quota q_{rank,e,.} exceeds j.  The send
+ * buffer holds one block per (destination rank t, physical slot p) in
+ * (t, p) order, block (t, p) holding q_{rank, e(t,p), t} rows in ascending
+ * token order.
+ *   x            [T][H] bf16 token rows of this rank
+ *   topk         [T][k] int32 expert ids (-1 = not routed)
+ *   plan         outputs of ultraep_plan (device buffers)
+ *   send         [T*k][H] bf16: routed rows at their positions, rows from
+ *                block_off[R*S] to T*k - 1 zero-filled
+ *   row_of_slot  [T*k] int32 row of send for each slot, -1 if not routed
+ *   block_off    [R*S + 1] int64 first row of each block, last = routed rows
+ *   ws           device workspace of ws_bytes >= ultraep_dispatch_ws_bytes
+ * A plan row that does not describe exactly the routed ids of topk raises
+ * ULTRAEP_EDATA. */
+int ultraep_dispatch(const uint16_t *x, const int32_t *topk, int64_t T,
+                     int32_t k, int32_t H, int32_t rank,
+                     const ultraep_group *g, const ultraep_plan_buf *plan,
+                     uint16_t *send, int32_t *row_of_slot, int64_t *block_off,
+                     void *ws, size_t ws_bytes, int32_t *status,
+                     hipStream_t stream);
+
+/* The two halves of ultraep_dispatch, for callers that move the rows
+ * themselves or time them apart: the layout (row_of_slot, block_off) and the
+ * scatter (send rows; n_routed = block_off + R * S, the routed row count). */
+int ultraep_dispatch_layout(const int32_t *topk, int64_t T, int32_t k,
+                            int32_t rank, const ultraep_group *g,
+                            const ultraep_plan_buf *plan, int32_t *row_of_slot,
+                            int64_t *block_off, void *ws, size_t ws_bytes,
+                            int32_t *status, hipStream_t stream);
+int ultraep_dispatch_scatter(const uint16_t *x, int64_t T, int32_t k,
+                             int32_t H, const int32_t *row_of_slot,
+                             const int64_t *n_routed, uint16_t *send,
+                             hipStream_t stream);
+
+/* Step 4 — local half of the forward weight distribution (Sec. 6.1; the
+ * remote peer stores are not part of this library).  Every redundant slot
+ * (t, s) whose expert e has home `rank` receives a bit copy of
+ * w_main[e - rank * n_main]; entries are ordered by destination rank t, then
+ * slot s.
+ *   w_main    [n_main][W] bf16 blobs of this rank's main experts (W elements
+ *             each; an expert's gate, up and down matrices as stored)
+ *   staging   [cap][W] bf16; entries 0 .. n_out-1 written, the rest untouched
+ *   dest_off  [R + 1] int64 first entry of each destination rank, last = n_out
+ * If n_out > cap, ULTRAEP_ENOSPC is raised, dest_off is still written and no
+ * entry is copied. */
+int ultraep_pack_replicas(const uint16_t *w_main, int64_t W, int32_t rank,
+                          const ultraep_group *g, const ultraep_plan_buf *plan,
+                          uint16_t *staging, int64_t cap, int64_t *dest_off,
+                          int32_t *status, hipStream_t stream);
+
+/* Host only.  Static description of a status code. */
+const char *ultraep_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ULTRAEP_H */

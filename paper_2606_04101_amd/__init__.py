@@ -1,0 +1,202 @@
+"""UltraEP per-microbatch balancing path for MI355X (gfx950).
+
+Thin ctypes binding of ``libultraep.so`` (C ABI in ``include/ultraep.h``).
+Every function has the name of the C entry point it calls and only marshals
+arguments: torch tensors supply device memory, torch's current HIP stream is
+used unless another one is given, and every step runs in the library's HIP
+kernels.  A missing library raises immediately; there is no fallback path.
+
+Reference: "UltraEP: Unleash MoE Training and Inference on Rack-Scale Nodes
+with Near-Optimal Load Balancing", arXiv 2606.04101 (Algorithm 1, Sec. 5-6).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libultraep.so")
+
+ULTRAEP_OK = 0
+ULTRAEP_EINVAL = -1
+ULTRAEP_ENOSPC = -2
+ULTRAEP_EDEVICE = -3
+ULTRAEP_EDATA = -4
+
+
+class UltraEPError(RuntimeError):
+    def __init__(self, code, where):
+        self.code = code
+        super().__init__(f"{where}: {ultraep_strerror(code)} ({code})")
+
+
+class Group(ctypes.Structure):
+    """ultraep_group: R ranks, E experts, n_slot redundant slots per rank,
+    quota floor u_min, balancing target beta_num / beta_den."""
+    _fields_ = [("R", ctypes.c_int32), ("E", ctypes.c_int32),
+                ("n_slot", ctypes.c_int32), ("u_min", ctypes.c_int64),
+                ("beta_num", ctypes.c_int32), ("beta_den", ctypes.c_int32)]
+
+    def __init__(self, R, E, n_slot, u_min, beta_num=101, beta_den=100):
+        super().__init__(R, E, n_slot, u_min, beta_num, beta_den)
+
+    @property
+    def n_main(self):
+        return self.E // self.R
+
+    @property
+    def S(self):
+        return self.n_main + self.n_slot
+
+    @property
+    def ncol(self):
+        return self.E + self.R * self.n_slot
+
+
+class PlanBuf(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("slot_expert", "quota", "host_ptr", "host_rank", "host_pslot",
+                 "reroute", "stats")]
+
+
+PLAN_FIELDS = ("slot_expert", "quota", "host_ptr", "host_rank", "host_pslot",
+               "reroute", "stats")
+
+_lib = None
+_P = ctypes.c_void_p
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        gp, pp = ctypes.POINTER(Group), ctypes.POINTER(PlanBuf)
+        L.ultraep_plan_sizes.argtypes = [gp, ctypes.POINTER(sz)]
+        L.ultraep_count.argtypes = [_P, i64, i32, i32, i32, _P, _P, _P]
+        L.ultraep_plan.argtypes = [_P, gp, pp, _P]
+        L.ultraep_dispatch_ws_bytes.argtypes = [i64, i32, gp]
+        L.ultraep_dispatch_ws_bytes.restype = sz
+        L.ultraep_dispatch.argtypes = [_P, _P, i64, i32, i32, i32, gp, pp, _P,
+                                       _P, _P, _P, sz, _P, _P]
+        L.ultraep_dispatch_layout.argtypes = [_P, i64, i32, i32, gp, pp, _P, _P,
+                                              _P, sz, _P, _P]
+        L.ultraep_dispatch_scatter.argtypes = [_P, i64, i32, i32, _P, _P, _P, _P]
+        L.ultraep_pack_replicas.argtypes = [_P, i64, i32, gp, pp, _P, i64, _P,
+                                            _P, _P]
+        L.ultraep_strerror.argtypes = [ctypes.c_int]
+        L.ultraep_strerror.restype = ctypes.c_char_p
+        for f in ("ultraep_plan_sizes", "ultraep_count", "ultraep_plan",
+                  "ultraep_dispatch", "ultraep_dispatch_layout",
+                  "ultraep_dispatch_scatter", "ultraep_pack_replicas"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def ultraep_strerror(code: int) -> str:
+    return lib().ultraep_strerror(int(code)).decode()
+
+
+def _check(rc, where):
+    if rc != ULTRAEP_OK:
+        raise UltraEPError(rc, where)
+    return rc
+
+
+def _ptr(t):
+    """Device address of a torch tensor (None for None / empty tensors)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr() if t.numel() else None
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def ultraep_plan_sizes(g: Group):
+    out = (ctypes.c_size_t * 7)()
+    _check(lib().ultraep_plan_sizes(ctypes.byref(g), out), "ultraep_plan_sizes")
+    return tuple(int(v) for v in out)
+
+
+class Plan:
+    """Device buffers of one plan (torch tensors) and their C descriptor."""
+
+    def __init__(self, g: Group, device="cuda"):
+        import torch
+        n = ultraep_plan_sizes(g)
+        dt = [torch.int32] * 6 + [torch.int64]
+        for name, cnt, d in zip(PLAN_FIELDS, n, dt):
+            setattr(self, name, torch.empty(cnt, dtype=d, device=device))
+        self.g = g
+        self.c = PlanBuf(*[_ptr(getattr(self, f)) for f in PLAN_FIELDS])
+
+
+def ultraep_count(topk, T, k, E, n_groups, counts, status, stream=None):
+    return _check(lib().ultraep_count(_ptr(topk), T, k, E, n_groups,
+                                      _ptr(counts), _ptr(status),
+                                      _stream(stream)), "ultraep_count")
+
+
+def ultraep_plan(load, g: Group, plan: Plan, stream=None):
+    return _check(lib().ultraep_plan(_ptr(load), ctypes.byref(g),
+                                     ctypes.byref(plan.c), _stream(stream)),
+                  "ultraep_plan")
+
+
+def ultraep_dispatch_ws_bytes(T, k, g: Group) -> int:
+    return int(lib().ultraep_dispatch_ws_bytes(T, k, ctypes.byref(g)))
+
+
+def ultraep_dispatch(x, topk, T, k, H, rank, g: Group, plan: Plan, send,
+                     row_of_slot, block_off, ws, status, stream=None):
+    return _check(lib().ultraep_dispatch(
+        _ptr(x), _ptr(topk), T, k, H, rank, ctypes.byref(g),
+        ctypes.byref(plan.c), _ptr(send), _ptr(row_of_slot), _ptr(block_off),
+        _ptr(ws), ws.numel() * ws.element_size(), _ptr(status),
+        _stream(stream)), "ultraep_dispatch")
+
+
+def ultraep_dispatch_layout(topk, T, k, rank, g: Group, plan: Plan,
+                            row_of_slot, block_off, ws, status, stream=None):
+    return _check(lib().ultraep_dispatch_layout(
+        _ptr(topk), T, k, rank, ctypes.byref(g), ctypes.byref(plan.c),
+        _ptr(row_of_slot), _ptr(block_off), _ptr(ws),
+        ws.numel() * ws.element_size(), _ptr(status), _stream(stream)),
+        "ultraep_dispatch_layout")
+
+
+def ultraep_dispatch_scatter(x, T, k, H, row_of_slot, n_routed, send,
+                             stream=None):
+    """n_routed: a one-element int64 device tensor (e.g. block_off[-1:])."""
+    return _check(lib().ultraep_dispatch_scatter(
+        _ptr(x), T, k, H, _ptr(row_of_slot), _ptr(n_routed), _ptr(send),
+        _stream(stream)), "ultraep_dispatch_scatter")
+
+
+def ultraep_pack_replicas(w_main, W, rank, g: Group, plan: Plan, staging, cap,
+                          dest_off, status, stream=None):
+    return _check(lib().ultraep_pack_replicas(
+        _ptr(w_main), W, rank, ctypes.byref(g), ctypes.byref(plan.c),
+        _ptr(staging), cap, _ptr(dest_off), _ptr(status), _stream(stream)),
+        "ultraep_pack_replicas")
+
+
+def build():
+    """Compile libultraep.so for gfx950 in-tree."""
+    from . import _build
+    global _lib
+    _lib = None
+    return _build.build()

@@ -1,0 +1,326 @@
+// Step 3 — token-to-replica assignment and dispatch permutation of one
+// source rank (Sec. 5.2 Token Assignment), then the bf16 row scatter.
+//
+// Layout (two launches, integer only):
+//   k_dl_hist  : workgroup c < n_chunks counts the expert ids of slots
+//                [c*2048, (c+1)*2048); the last workgroup turns row `rank` of
+//                the reroute split into block sizes (t, p), their exclusive
+//                prefix block_off, and per CSR entry the cumulative quota C
+//                and the first row minus the entry's starting ordinal.
+//   k_dl_rows  : workgroup c sums the histograms of chunks < c (its base
+//                ordinal per expert), then each wave ranks its 128 slots
+//                stably with ballot matches (wave-private running counts in
+//                LDS, scanned across waves), finds the first instance whose
+//                cumulative quota exceeds the ordinal and writes the row.
+// Scatter (bandwidth bound): one wave per token reads the token's row once
+//   into registers with 16-byte loads and stores it to each of its k
+//   destination rows with 16-byte non-temporal stores; rows past the routed
+//   count are zero-filled.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace uep {
+
+constexpr int kDlThreads = 1024;
+constexpr int kDlWaves = kDlThreads / kWave;
+constexpr int kSlotsPerWave = kDispatchChunk / kDlWaves;  // 128
+constexpr int kMaxBlocks = 2048;                           // R * S
+
+static_assert(kSlotsPerWave % kWave == 0, "chunk must split into wave steps");
+
+size_t dispatch_ws_bytes(int64_t V, int32_t E, int32_t ncol) {
+  const int64_t n_chunks = (V + kDispatchChunk - 1) / kDispatchChunk;
+  const int64_t ints = n_chunks * E + 2 * static_cast<int64_t>(ncol) + E;
+  return static_cast<size_t>((ints * 4 + 255) / 256 * 256);
+}
+
+DispatchWs dispatch_ws(void *ws, int64_t V, int32_t E, int32_t ncol) {
+  DispatchWs w;
+  w.n_chunks = (V + kDispatchChunk - 1) / kDispatchChunk;
+  int32_t *p = static_cast<int32_t *>(ws);
+  w.hist = p;
+  p += w.n_chunks * E;
+  w.ent_cum = p;
+  p += ncol;
+  w.ent_base = p;
+  p += ncol;
+  w.exp_tot = p;
+  return w;
+}
+
+struct DlArgs {
+  const int32_t *topk;
+  int64_t V;
+  int32_t rank, R, E, NS, nm, S, ncol, nbits;
+  const int32_t *hp, *hr, *hs, *q;  // q = reroute row of `rank`
+  int32_t *row_of_slot;
+  int64_t *block_off;
+  DispatchWs ws;
+  int32_t *status;
+};
+
+__global__ void __launch_bounds__(kDlThreads) k_dl_hist(DlArgs a) {
+  extern __shared__ int32_t lds[];
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int E = a.E;
+  if (blockIdx.x < a.ws.n_chunks) {
+    int32_t *hist = lds;  // [kDlWaves][E]
+    for (int i = tid; i < kDlWaves * E; i += kDlThreads) hist[i] = 0;
+    __syncthreads();
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kDispatchChunk;
+    int32_t *wh = hist + wave * E;
+    bool bad = false;
+    for (int s = 0; s < kSlotsPerWave; s += kWave) {
+      const int64_t i = c0 + wave * kSlotsPerWave + s + lane;
+      const int32_t e = i < a.V ? a.topk[i] : -1;
+      const bool valid = e >= 0 && e < E;
+      bad |= (i < a.V) && (e < -1 || e >= E);
+      const uint64_t act = ballot(valid);
+      if (act == 0) continue;
+      const uint64_t m = match_any(static_cast<uint32_t>(valid ? e : 0), a.nbits, act);
+      if (valid && popc_below(m) == 0) wh[e] += __popcll(m);
+    }
+    if (bad) report(a.status, ULTRAEP_EDATA);
+    __syncthreads();
+    int32_t *dst = a.ws.hist + blockIdx.x * static_cast<int64_t>(E);
+    for (int e = tid; e < E; e += kDlThreads) {
+      int s = 0;
+      for (int w = 0; w < kDlWaves; ++w) s += hist[w * E + e];
+      dst[e] = s;
+    }
+    return;
+  }
+  // ---- layout workgroup: block sizes, offsets, entry lookup tables ----
+  int32_t *cnt = lds;  // [R*S]
+  int32_t *tmp = lds + kMaxBlocks;
+  const int nblk = a.R * a.S;
+  for (int b = tid; b < nblk; b += kDlThreads) cnt[b] = 0;
+  __syncthreads();
+  const int total = a.hp[E];
+  if (total < E || total > a.ncol) {  // not a plan of this group
+    if (tid == 0) report(a.status, ULTRAEP_EDATA);
+    return;
+  }
+  for (int j = tid; j < total; j += kDlThreads) {
+    const int t = a.hr[j], p = a.hs[j];
+    if (t >= 0 && t < a.R && p >= 0 && p < a.S) cnt[t * a.S + p] = a.q[j];
+    else report(a.status, ULTRAEP_EDATA);
+  }
+  __syncthreads();
+  // exclusive scan of cnt (two elements per thread) into int64 offsets
+  const int b0 = 2 * tid, b1 = 2 * tid + 1;
+  const int v0 = b0 < nblk ? cnt[b0] : 0, v1 = b1 < nblk ? cnt[b1] : 0;
+  int incl = v0 + v1;
+  for (int o = 1; o < kWave; o <<= 1) {
+    int t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  if (lane == kWave - 1) tmp[wave] = incl;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int w = 0; w < kDlWaves; ++w) {
+      int t = tmp[w];
+      tmp[w] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+  const int ex0 = tmp[wave] + incl - v0 - v1;
+  __syncthreads();
+  // reuse cnt as offsets
+  if (b0 < nblk) cnt[b0] = ex0;
+  if (b1 < nblk) cnt[b1] = ex0 + v0;
+  if (b0 < nblk) a.block_off[b0] = ex0;
+  if (b1 < nblk) a.block_off[b1] = ex0 + v0;
+  if (b1 == nblk || b0 == nblk) a.block_off[nblk] = ex0 + (b0 == nblk ? 0 : v0);
+  __syncthreads();
+  for (int e = tid; e < E; e += kDlThreads) {
+    int C = 0;
+    for (int j = a.hp[e]; j < a.hp[e + 1]; ++j) {
+      const int t = a.hr[j], p = a.hs[j];
+      const bool ok = t >= 0 && t < a.R && p >= 0 && p < a.S;
+      a.ws.ent_base[j] = (ok ? cnt[t * a.S + p] : 0) - C;
+      C += a.q[j];
+      a.ws.ent_cum[j] = C;
+    }
+    a.ws.exp_tot[e] = C;
+  }
+}
+
+__global__ void __launch_bounds__(kDlThreads) k_dl_rows(DlArgs a) {
+  extern __shared__ int32_t lds[];
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int E = a.E;
+  const int c = blockIdx.x;
+  int32_t *whist = lds;  // [kDlWaves][E]
+  int32_t *base = lds + kDlWaves * E;
+  for (int e = tid; e < E; e += kDlThreads) {
+    int s = 0;
+    for (int cc = 0; cc < c; ++cc) s += a.ws.hist[cc * static_cast<int64_t>(E) + e];
+    base[e] = s;
+    if (c == 0) {
+      int tot = 0;
+      for (int cc = 0; cc < a.ws.n_chunks; ++cc) tot += a.ws.hist[cc * static_cast<int64_t>(E) + e];
+      if (tot != a.ws.exp_tot[e]) report(a.status, ULTRAEP_EDATA);
+    }
+  }
+  for (int i = tid; i < kDlWaves * E; i += kDlThreads) whist[i] = 0;
+  __syncthreads();
+  const int64_t s0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kSlotsPerWave;
+  int32_t *wh = whist + wave * E;
+  // pass 1: per-wave counts
+  for (int s = 0; s < kSlotsPerWave; s += kWave) {
+    const int64_t i = s0 + s + lane;
+    const int32_t e = i < a.V ? a.topk[i] : -1;
+    const bool valid = e >= 0 && e < E;
+    const uint64_t act = ballot(valid);
+    if (act == 0) continue;
+    const uint64_t m = match_any(static_cast<uint32_t>(valid ? e : 0), a.nbits, act);
+    if (valid && popc_below(m) == 0) wh[e] += __popcll(m);
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += kDlThreads) {
+    int run = base[e];
+    for (int w = 0; w < kDlWaves; ++w) {
+      int t = whist[w * E + e];
+      whist[w * E + e] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+  // pass 2: stable ordinals, instance lookup, rows
+  for (int s = 0; s < kSlotsPerWave; s += kWave) {
+    const int64_t i = s0 + s + lane;
+    const int32_t e = i < a.V ? a.topk[i] : -1;
+    const bool valid = e >= 0 && e < E;
+    const uint64_t act = ballot(valid);
+    if (act == 0) {
+      if (i < a.V) a.row_of_slot[i] = -1;
+      continue;
+    }
+    const uint64_t m = match_any(static_cast<uint32_t>(valid ? e : 0), a.nbits, act);
+    int row = -1;
+    if (valid) {
+      const int below = popc_below(m);
+      const int ord = wh[e] + below;
+      if (below == 0) wh[e] += __popcll(m);
+      const int j1 = a.hp[e + 1];
+      int j = a.hp[e];
+      while (j < j1 && a.ws.ent_cum[j] <= ord) ++j;
+      if (j < j1) row = a.ws.ent_base[j] + ord;
+      // a plan row that does not match these ids can point past the buffer
+      if (row < 0 || row >= a.V) {
+        row = -1;
+        report(a.status, ULTRAEP_EDATA);
+      }
+    }
+    if (i < a.V) a.row_of_slot[i] = row;
+  }
+}
+
+hipError_t launch_dispatch_layout(const int32_t *topk, int64_t V, int32_t rank,
+                                  const ultraep_group &g,
+                                  const ultraep_plan_buf &plan,
+                                  int32_t *row_of_slot, int64_t *block_off,
+                                  const DispatchWs &ws, int32_t *status,
+                                  hipStream_t stream) {
+  DlArgs a;
+  a.topk = topk;
+  a.V = V;
+  a.rank = rank;
+  a.R = g.R;
+  a.E = g.E;
+  a.NS = g.n_slot;
+  a.nm = g.E / g.R;
+  a.S = a.nm + g.n_slot;
+  a.ncol = g.E + g.R * g.n_slot;
+  a.nbits = bits_for(g.E);
+  a.hp = plan.host_ptr;
+  a.hr = plan.host_rank;
+  a.hs = plan.host_pslot;
+  a.q = plan.reroute + static_cast<int64_t>(rank) * a.ncol;
+  a.row_of_slot = row_of_slot;
+  a.block_off = block_off;
+  a.ws = ws;
+  a.status = status;
+  const size_t lds_hist = sizeof(int32_t) * kDlWaves * g.E;
+  const size_t lds_lay = sizeof(int32_t) * (kMaxBlocks + kDlWaves + 1);
+  hipLaunchKernelGGL(k_dl_hist, dim3(ws.n_chunks + 1), dim3(kDlThreads),
+                     lds_hist > lds_lay ? lds_hist : lds_lay, stream, a);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || ws.n_chunks == 0) return err;
+  hipLaunchKernelGGL(k_dl_rows, dim3(ws.n_chunks), dim3(kDlThreads),
+                     sizeof(int32_t) * (kDlWaves + 1) * g.E, stream, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- scatter
+
+constexpr int kScThreads = 256;
+constexpr int kScWaves = kScThreads / kWave;
+
+template <int U>
+__global__ void __launch_bounds__(kScThreads)
+k_scatter(const v4u *__restrict__ x, int64_t T, int32_t k, int32_t nch,
+          const int32_t *__restrict__ row_of_slot, const int64_t *n_routed,
+          v4u *__restrict__ send) {
+  const int lane = lane_id();
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * kScWaves + threadIdx.x / kWave;
+  if (t < T) {
+    const int rows = lane < k ? row_of_slot[t * k + lane] : -1;
+    const v4u *src = x + t * nch;
+    for (int c0 = 0; c0 < nch; c0 += U * kWave) {
+      v4u v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int cc = c0 + u * kWave + lane;
+        if (cc < nch) v[u] = __builtin_nontemporal_load(src + cc);
+      }
+      for (int kk = 0; kk < k; ++kk) {
+        const int row = readlane(rows, kk);
+        if (row < 0 || row >= T * k) continue;
+        v4u *dst = send + static_cast<int64_t>(row) * nch;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int cc = c0 + u * kWave + lane;
+          if (cc < nch) __builtin_nontemporal_store(v[u], dst + cc);
+        }
+      }
+    }
+  }
+  // rows after the routed ones (masked slots) are zero-filled
+  const int64_t V = T * k;
+  const int64_t nr = *n_routed;
+  if (nr < V) {
+    const int64_t gw = static_cast<int64_t>(blockIdx.x) * kScWaves + threadIdx.x / kWave;
+    const int64_t nw = static_cast<int64_t>(gridDim.x) * kScWaves;
+    const v4u z = v4u{0u, 0u, 0u, 0u};
+    for (int64_t row = nr + gw; row < V; row += nw)
+      for (int cc = lane; cc < nch; cc += kWave) send[row * nch + cc] = z;
+  }
+}
+
+hipError_t launch_dispatch_scatter(const uint16_t *x, int64_t T, int32_t k,
+                                   int32_t H, const int32_t *row_of_slot,
+                                   const int64_t *n_routed, uint16_t *send,
+                                   hipStream_t stream) {
+  const int32_t nch = H / 8;
+  const dim3 grid(static_cast<unsigned>((T + kScWaves - 1) / kScWaves));
+  const int per_lane = (nch + kWave - 1) / kWave;
+  const v4u *xs = reinterpret_cast<const v4u *>(x);
+  v4u *sd = reinterpret_cast<v4u *>(send);
+  if (per_lane <= 1)
+    hipLaunchKernelGGL(k_scatter<1>, grid, dim3(kScThreads), 0, stream, xs, T, k, nch, row_of_slot, n_routed, sd);
+  else if (per_lane <= 2)
+    hipLaunchKernelGGL(k_scatter<2>, grid, dim3(kScThreads), 0, stream, xs, T, k, nch, row_of_slot, n_routed, sd);
+  else if (per_lane <= 4)
+    hipLaunchKernelGGL(k_scatter<4>, grid, dim3(kScThreads), 0, stream, xs, T, k, nch, row_of_slot, n_routed, sd);
+  else if (per_lane <= 8)
+    hipLaunchKernelGGL(k_scatter<8>, grid, dim3(kScThreads), 0, stream, xs, T, k, nch, row_of_slot, n_routed, sd);
+  else
+    hipLaunchKernelGGL(k_scatter<16>, grid, dim3(kScThreads), 0, stream, xs, T, k, nch, row_of_slot, n_routed, sd);
+  return hipGetLastError();
+}
+
+}  // namespace uep

@@ -1,0 +1,91 @@
+"""The C ABI library loads, exports every entry point include/ultraep.h
+declares, and rejects bad host-visible arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_04101_amd as uep
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "ultraep.h")
+
+
+def declared_symbols():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ultraep_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_symbols()
+    for n in ("ultraep_count", "ultraep_plan", "ultraep_dispatch",
+              "ultraep_pack_replicas", "ultraep_plan_sizes",
+              "ultraep_dispatch_ws_bytes", "ultraep_strerror"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(uep.LIB_PATH)
+    missing = [n for n in declared_symbols() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_plan_sizes():
+    g = uep.Group(64, 256, 1, 1024)
+    assert uep.ultraep_plan_sizes(g) == (64, 256 * 64, 257, 320, 320, 64 * 320, 8)
+    for bad in [uep.Group(3, 8, 1, 1), uep.Group(65, 65, 1, 1),
+                uep.Group(4, 2048, 1, 1), uep.Group(4, 8, -1, 1),
+                uep.Group(4, 8, 65, 1), uep.Group(4, 8, 1, 0),
+                uep.Group(4, 8, 1, 1, 99, 100), uep.Group(4, 8, 1, 1, 1, 0)]:
+        with pytest.raises(uep.UltraEPError):
+            uep.ultraep_plan_sizes(bad)
+
+
+def test_ws_bytes():
+    g = uep.Group(64, 256, 1, 1024)
+    n = uep.ultraep_dispatch_ws_bytes(4096, 8, g)
+    assert n >= 4 * (16 * 256 + 2 * 320 + 256) and n % 256 == 0
+    assert uep.ultraep_dispatch_ws_bytes(-1, 8, g) == 0
+    assert uep.ultraep_dispatch_ws_bytes(10, 0, g) == 0
+    assert uep.ultraep_dispatch_ws_bytes(10, 300, g) == 0
+
+
+def test_invalid_arguments_return_einval_without_launch():
+    L = uep.lib()
+    g = uep.Group(4, 16, 2, 32)
+    pb = uep.PlanBuf(*([None] * 7))
+    fake = ctypes.c_void_p(4096)  # never dereferenced: validation fails first
+    E = uep.ULTRAEP_EINVAL
+    assert L.ultraep_count(fake, 8, 2, 16, 1, None, fake, None) == E      # no counts
+    assert L.ultraep_count(fake, 8, 0, 16, 1, fake, fake, None) == E      # k = 0
+    assert L.ultraep_count(fake, 8, 17, 16, 1, fake, fake, None) == E     # k > E
+    assert L.ultraep_count(fake, 8, 2, 16, 0, fake, fake, None) == E      # no groups
+    assert L.ultraep_count(fake, 8, 2, 16, 1, fake, None, None) == E      # no status
+    assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(pb), None) == E
+    bad = uep.Group(4, 15, 2, 32)
+    full = uep.PlanBuf(*([4096] * 7))
+    assert L.ultraep_plan(fake, ctypes.byref(bad), ctypes.byref(full), None) == E
+    assert L.ultraep_dispatch(fake, fake, 8, 2, 12, 0, ctypes.byref(g),  # H % 8
+                              ctypes.byref(full), fake, fake, fake, fake, 1 << 20,
+                              fake, None) == E
+    assert L.ultraep_dispatch(fake, fake, 8, 2, 16, 4, ctypes.byref(g),  # rank >= R
+                              ctypes.byref(full), fake, fake, fake, fake, 1 << 20,
+                              fake, None) == E
+    assert L.ultraep_dispatch(fake, fake, 8, 2, 16, 0, ctypes.byref(g),  # small ws
+                              ctypes.byref(full), fake, fake, fake, fake, 16,
+                              fake, None) == E
+    odd = ctypes.c_void_p(4096 + 4)
+    assert L.ultraep_dispatch_scatter(odd, 8, 2, 16, fake, fake, fake, None) == E
+    assert L.ultraep_pack_replicas(fake, 12, 0, ctypes.byref(g), ctypes.byref(full),
+                                   fake, 4, fake, fake, None) == E     # W % 8
+    assert L.ultraep_pack_replicas(fake, 16, 0, ctypes.byref(g), ctypes.byref(full),
+                                   fake, -1, fake, fake, None) == E    # cap < 0
+    assert L.ultraep_pack_replicas(fake, 16, 0, ctypes.byref(g), ctypes.byref(full),
+                                   odd, 4, fake, fake, None) == E      # misaligned
+
+
+def test_strerror():
+    assert uep.ultraep_strerror(0) == "ok"
+    assert "capacity" in uep.ultraep_strerror(uep.ULTRAEP_ENOSPC)

@@ -1,0 +1,241 @@
+"""Parity of the HIP library with the oracle, byte for byte, on the same seeded
+inputs: the five synthetic workloads at full size, every simulated rank of the
+tiny workload, the adversarial fuzz corpus, error paths, determinism and
+HIP-graph replay.  Needs an MI355X."""
+import numpy as np
+import pytest
+import torch
+
+import fuzz
+import gen
+import oracle
+from invariants import check_plan
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import gpu_path as gp
+    import paper_2606_04101_amd as uep
+
+
+def _workload(cid, m):
+    c = gen.config(cid)
+    g, og = gp.groups(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+    return c, g, og, gen.topk_all(c, m)
+
+
+def _rstar(op, c):
+    X = op.slot_expert
+    outb = [int(((X >= 0) & (X // c.n_main == r)).sum()) for r in range(c.R)]
+    return int(np.argmax(outb))
+
+
+# ------------------------------------------------------------- count + plan
+
+@pytest.mark.parametrize("cid,m", [(1, 0), (1, 3), (2, 0), (3, 0), (3, 7),
+                                   (3, 15), (4, 0), (4, 1), (5, 0), (5, 57)])
+def test_count_and_plan_workloads(cid, m):
+    c, g, og, tk = _workload(cid, m)
+    counts, st = gp.gpu_count(tk, c.E)
+    ocounts, ost = oracle.count(tk, c.E, c.R)
+    assert st == 0 and ost == 0
+    assert np.array_equal(counts, ocounts)
+    plan = gp.gpu_plan(ocounts, g)
+    op = oracle.plan(ocounts, og)
+    gp.assert_plan_equal(plan, op)
+    check_plan(ocounts, og, op)
+
+
+def test_qwen3_all_microbatches():
+    c = gen.config(3)
+    g, og = gp.groups(c.R, c.E, c.n_slot, c.u_min)
+    for m in range(c.n_micro):
+        tk = gen.topk_all(c, m)
+        counts, st = gp.gpu_count(tk, c.E)
+        assert st == 0
+        gp.assert_plan_equal(gp.gpu_plan(counts, g), oracle.plan(counts, og))
+
+
+def test_dsv3_prefill_all_layers_plan():
+    c = gen.config(5)
+    g, og = gp.groups(c.R, c.E, c.n_slot, c.u_min)
+    for layer in range(c.n_micro):
+        tk = gen.topk_all(c, layer)
+        counts, st = gp.gpu_count(tk, c.E)
+        assert st == 0
+        gp.assert_plan_equal(gp.gpu_plan(counts, g), oracle.plan(counts, og))
+
+
+# ------------------------------------------------------------- dispatch + pack
+
+def test_tiny_every_rank():
+    c, g, og, tk = _workload(1, 0)
+    load, _ = oracle.count(tk, c.E, c.R)
+    op = oracle.plan(load, og)
+    plan = gp.gpu_plan(load, g)
+    for r in range(c.R):
+        x = gen.activations(c, 0, r)
+        w = gen.weights(c, r)
+        gp.check_rank(x, tk[r], w, r, g, og, plan, op)
+
+
+@pytest.mark.parametrize("cid,m", [(2, 0), (3, 0), (4, 0), (5, 0)])
+def test_full_size_dispatch_and_pack(cid, m):
+    """Full-size rows (H) and expert blobs (W_e) for ranks 0, the rank with
+    the most outbound replicas, and R-1."""
+    c, g, og, tk = _workload(cid, m)
+    load, _ = oracle.count(tk, c.E, c.R)
+    op = oracle.plan(load, og)
+    plan = gp.gpu_plan(load, g)
+    rs = sorted({0, _rstar(op, c), c.R - 1})
+    for r in rs:
+        x = gen.activations(c, m, r)
+        w = gen.weights(c, r) if r == rs[0] or r == _rstar(op, c) else None
+        gp.check_rank(x, tk[r], w, r, g, og, plan, op, split=(r == rs[-1]))
+
+
+@pytest.mark.parametrize("seed", range(0, 160))
+def test_fuzz_parity(seed):
+    case = fuzz.make_case(seed)
+    g, og = gp.groups(case["R"], case["E"], case["n_slot"], case["u_min"],
+                      case["beta_num"], case["beta_den"])
+    tk = case["topk"]
+    if tk.shape[1] > 0:
+        counts, st = gp.gpu_count(tk, g.E)
+        ocounts, _ = oracle.count(tk, g.E, g.R)
+        assert st == 0 and np.array_equal(counts, ocounts)
+    else:
+        ocounts = np.zeros((g.R, g.E), np.int32)
+    op = oracle.plan(ocounts, og)
+    plan = gp.gpu_plan(ocounts, g)
+    gp.assert_plan_equal(plan, op)
+    rng = case["rng"]
+    for r in sorted({0, g.R - 1}):
+        x = rng.integers(0, 2 ** 16, (case["T"], case["H"])).astype(np.uint16)
+        w = rng.integers(0, 2 ** 16, (g.n_main, case["W"])).astype(np.uint16)
+        gp.check_rank(x, tk[r], w, r, g, og, plan, op, split=bool(seed % 2))
+
+
+# ------------------------------------------------------------- error paths
+
+def test_count_flags_bad_ids():
+    tk = np.array([[[0, 3], [16, -1]], [[-2, 1], [2, 2]]], np.int32)
+    counts, st = gp.gpu_count(tk, 16)
+    assert st == uep.ULTRAEP_EDATA
+    assert counts[0].tolist()[:4] == [1, 0, 0, 1] and counts[1].tolist()[:3] == [0, 1, 2]
+
+
+def test_plan_flags_negative_load():
+    g, og = gp.groups(4, 8, 1, 1)
+    load = np.ones((4, 8), np.int32)
+    load[2, 5] = -3
+    plan = gp.gpu_plan(load, g)
+    assert int(plan.stats[6].item()) == uep.ULTRAEP_EDATA
+
+
+def test_dispatch_flags_plan_mismatch():
+    g, og = gp.groups(4, 8, 1, 1)
+    load = np.ones((4, 8), np.int32)
+    plan = gp.gpu_plan(load, g)
+    x = np.zeros((2, 8), np.uint16)
+    _, _, _, st = gp.gpu_dispatch(x, np.array([[0, 1], [2, 3]], np.int32), 0, g, plan)
+    assert st == uep.ULTRAEP_EDATA
+
+
+def test_pack_flags_small_capacity():
+    g, og = gp.groups(4, 8, 1, 1)
+    load = np.zeros((4, 8), np.int32)
+    load[0, 0] = 100
+    op = oracle.plan(load, og)
+    plan = gp.gpu_plan(load, g)
+    n = int(op.stats[4])
+    assert n >= 2
+    w = np.arange(2 * 16, dtype=np.uint16).reshape(2, 16)
+    stg, doff, st = gp.gpu_pack(w, 0, g, plan, n - 1)
+    assert st == uep.ULTRAEP_ENOSPC
+    _, odoff, _, _ = oracle.pack(w, 0, og, op, n)
+    assert np.array_equal(doff, odoff)
+    assert (stg == 0x3C3C).all()
+
+
+def test_host_argument_errors_raise():
+    g, _ = gp.groups(3, 8, 1, 1)  # E % R != 0
+    with pytest.raises(uep.UltraEPError) as ei:
+        uep.ultraep_plan_sizes(g)
+    assert ei.value.code == uep.ULTRAEP_EINVAL
+
+
+# ------------------------------------------------------------- determinism, graphs
+
+def test_repeated_runs_identical():
+    c, g, og, tk = _workload(4, 0)
+    load, _ = oracle.count(tk, c.E, c.R)
+    ref = gp.gpu_plan(load, g)
+    ref_h = {f: getattr(ref, f).cpu().numpy() for f in uep.PLAN_FIELDS}
+    for _ in range(20):
+        p = gp.gpu_plan(load, g)
+        for f in uep.PLAN_FIELDS:
+            assert np.array_equal(getattr(p, f).cpu().numpy(), ref_h[f])
+    r = 5
+    x = gen.activations(c, 0, r)
+    a = gp.gpu_dispatch(x, tk[r], r, g, ref)
+    for _ in range(3):
+        b = gp.gpu_dispatch(x, tk[r], r, g, ref, split=True)
+        assert a[3] == b[3] == 0
+        assert all(np.array_equal(u, v) for u, v in zip(a[:3], b[:3]))
+
+
+def test_graph_replay_matches_eager():
+    """count -> plan -> dispatch -> pack captured in one HIP graph, replayed
+    several times with eager work in between; every replay must equal the
+    eager result."""
+    c, g, og, tk_all = _workload(1, 2)
+    r = 2
+    T, k, H = c.T, c.k, c.H
+    W = 3 * c.H * 32
+    x = gp.dev_u16(gen.activations(c, 2, r))
+    w = gp.dev_u16(gen.weights(c, r, W=W))
+    tk_all_d = gp.dev_i32(tk_all)
+    tk_r = tk_all_d[r].contiguous()
+    load = torch.empty((c.R, c.E), dtype=torch.int32, device=gp.DEV)
+    st = gp.zero_status()
+    plan = uep.Plan(g, gp.DEV)
+    V = T * k
+    send = torch.empty((V, H), dtype=torch.int16, device=gp.DEV)
+    ros = torch.empty(V, dtype=torch.int32, device=gp.DEV)
+    boff = torch.empty(c.R * g.S + 1, dtype=torch.int64, device=gp.DEV)
+    ws = torch.empty(uep.ultraep_dispatch_ws_bytes(T, k, g), dtype=torch.uint8, device=gp.DEV)
+    cap = c.R * c.n_slot
+    stg = torch.zeros((cap, W), dtype=torch.int16, device=gp.DEV)
+    doff = torch.empty(c.R + 1, dtype=torch.int64, device=gp.DEV)
+
+    def step():
+        uep.ultraep_count(tk_all_d, T, k, c.E, c.R, load, st)
+        uep.ultraep_plan(load, g, plan)
+        uep.ultraep_dispatch(x, tk_r, T, k, H, r, g, plan, send, ros, boff, ws, st)
+        uep.ultraep_pack_replicas(w, W, r, g, plan, stg, cap, doff, st)
+
+    outs = lambda: [t.clone() for t in (load, send, ros, boff, stg, doff,
+                                        *[getattr(plan, f) for f in uep.PLAN_FIELDS])]
+    step()
+    torch.cuda.synchronize()
+    ref = outs()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for i in range(4):
+        for t in (load, send, ros, boff, doff, *[getattr(plan, f) for f in uep.PLAN_FIELDS]):
+            t.fill_(-1)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = outs()
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), f"replay {i} differs"
+        assert int(st.item()) == 0
