@@ -1,0 +1,300 @@
+#!/usr/bin/env python3
+"""Benchmark of the UltraEP per-layer balancing path on one MI355X.
+
+One step = one layer-microbatch of the hot path on the measured rank:
+  count  (that rank's top-k ids -> its row of the load matrix)
+  plan   (SolveReplication + SolveReroute over the whole EP group)
+  dispatch layout + row scatter (bf16 rows into per-replica send blocks)
+  pack   (replicated main-expert blobs into per-destination staging)
+on synthetic DeepSeek-V3-shaped training routing (E=256, top-8 with
+8-group / top-4-group restriction, EP=64, one redundant slot per rank,
+4096 tokens per rank, H=7168, F=2048).  The other 63 ranks' load rows are
+resident inputs (the all-gather that delivers them is not on one GPU).  The
+measured rank is the one with the most outbound replica bytes.
+
+Timed region: K replays of the step captured in one HIP graph, bracketed by
+device synchronisation.  A second pass of K eager steps records HIP events
+around every launch on the launch stream; the dominant kernel's average
+duration gives the roofline figures.  The CPU oracle is timed
+single-threaded on a bounded sample of the same workload.
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("plan+dispatch latency per layer-microbatch (µs); "
+          "dispatch/pack HBM GB/s vs peak")
+PEAK_HBM_GBPS = 8000.0
+WORKLOAD_ID = 4
+
+
+def kernel_source_digest(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2606_04101_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, digest):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 PMC
+    summary, or None if absent or taken on different kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f).get(kernel)
+    if not d or d.get("source_digest") != digest:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the "
+              "balancing path is replicated per rank and its collectives are not "
+              "part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2606_04101_amd as uep
+
+    dev = torch.device("cuda:0")
+    c = gen.config(WORKLOAD_ID)
+    g = uep.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+    T, k, H, W = c.T, c.k, c.H, c.W
+    V = T * k
+
+    # ---------------- inputs (generated on the host, uploaded once)
+    t0 = time.time()
+    tk_all = gen.topk_all(c, 0)
+    tk_all_d = torch.from_numpy(tk_all).to(dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    load = torch.empty((c.R, c.E), dtype=torch.int32, device=dev)
+    uep.ultraep_count(tk_all_d, T, k, c.E, c.R, load, status)  # every rank's row
+    plan = uep.Plan(g, dev)
+    uep.ultraep_plan(load, g, plan)
+    torch.cuda.synchronize()
+    X = plan.slot_expert.cpu().numpy().reshape(c.R, c.n_slot)
+    n_out_r = [int(((X >= 0) & (X // c.n_main == r)).sum()) for r in range(c.R)]
+    rank = int(np.argmax(n_out_r))  # ties -> smallest rank
+    fan = np.bincount(X[(X >= 0) & (X // c.n_main == rank)] - rank * c.n_main,
+                      minlength=c.n_main)
+    x_h = gen.activations(c, 0, rank)
+    w_h = gen.weights(c, rank)
+    x = torch.from_numpy(x_h.view(np.int16)).to(dev)
+    w = torch.from_numpy(w_h.view(np.int16)).to(dev)
+    topk_r = tk_all_d[rank].contiguous()
+    load_r = load[rank]
+    send = torch.empty((V, H), dtype=torch.int16, device=dev)
+    ros = torch.empty(V, dtype=torch.int32, device=dev)
+    boff = torch.empty(c.R * g.S + 1, dtype=torch.int64, device=dev)
+    ws = torch.empty(uep.ultraep_dispatch_ws_bytes(T, k, g), dtype=torch.uint8, device=dev)
+    cap = max(1, n_out_r[rank])
+    staging = torch.empty((cap, W), dtype=torch.int16, device=dev)
+    doff = torch.empty(c.R + 1, dtype=torch.int64, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    calls = [
+        ("count", lambda: uep.ultraep_count(topk_r, T, k, c.E, 1, load_r, status)),
+        ("plan", lambda: uep.ultraep_plan(load, g, plan)),
+        ("dispatch_layout", lambda: uep.ultraep_dispatch_layout(
+            topk_r, T, k, rank, g, plan, ros, boff, ws, status)),
+        ("dispatch_scatter", lambda: uep.ultraep_dispatch_scatter(
+            x, T, k, H, ros, boff[-1:], send)),
+        ("pack", lambda: uep.ultraep_pack_replicas(
+            w, W, rank, g, plan, staging, cap, doff, status)),
+    ]
+
+    def step():
+        for _, f in calls:
+            f()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---------------- timed region: K graph replays of the whole step
+    graph = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(max(1, args.warmup)):
+        graph.replay()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    t_graph = (time.perf_counter() - t_start) / args.steps
+
+    # ---------------- eager pass with HIP events around every launch
+    stream = torch.cuda.current_stream()
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in calls] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        for (name, f), (e0, e1) in zip(calls, evs[i]):
+            e0.record(stream)
+            f()
+            e1.record(stream)
+    torch.cuda.synchronize()
+    t_eager = (time.perf_counter() - t_start) / args.steps
+    per_call_us = {name: 1e3 * float(np.mean([evs[i][j][0].elapsed_time(evs[i][j][1])
+                                              for i in range(args.steps)]))
+                   for j, (name, _) in enumerate(calls)}
+    st = int(status.item())
+    assert st == 0, f"device status {st}: {uep.ultraep_strerror(st)}"
+    n_routed = int(boff[-1].item())
+
+    # ---------------- a plain copy of known size (achievable bandwidth and
+    # the reference kernel for scaling the HBM byte counters)
+    a = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 2 * a.numel() * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+
+    # ---------------- algorithmic bytes per launch
+    scatter_bytes = 2 * T * H + 2 * n_routed * H + 4 * V
+    W_bytes = 2 * W
+    pack_bytes = int(sum(W_bytes * (1 + f) for f in fan if f > 0))
+    kern = {
+        "dispatch_scatter": (scatter_bytes, per_call_us["dispatch_scatter"],
+                             ["dispatch.hip", "common.hpp"]),
+        "pack": (pack_bytes, per_call_us["pack"], ["pack.hip", "common.hpp"]),
+    }
+    dom = max(kern, key=lambda n: kern[n][1])
+    dbytes, dus, dsrc = kern[dom]
+    achieved = dbytes / (dus * 1e-6) / 1e9
+    traffic = load_traffic(dom, kernel_source_digest(dsrc))
+
+    out = {
+        "metric": METRIC,
+        "value": round(t_graph * 1e6, 2),
+        "unit": "µs",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_graph * 1e3, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{c.name}: DeepSeek-V3-shaped layer, E={c.E} top-{c.k} "
+                         f"({c.n_group}-group/top-{c.top_group}), R={c.R} simulated "
+                         f"ranks, n_slot={c.n_slot}, T={T} tokens/rank, H={H}, "
+                         f"F={c.F}, bf16 rows and expert blobs (bit copies); "
+                         f"measured rank {rank}"),
+            "rank": rank,
+            "tokens_per_rank": T,
+            "routed_rows": n_routed,
+            "replicas_shipped": int(n_out_r[rank]),
+            "expert_blob_bytes": W_bytes,
+            "timed": "HIP graph replay of count+plan+dispatch+pack",
+        },
+        "roofline": {
+            "kernel": dom,
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": dbytes,
+            "avg_launch_us": round(dus, 2),
+        },
+        "kernels_us": {n: round(v, 2) for n, v in per_call_us.items()},
+        "count_plan_us": round(per_call_us["count"] + per_call_us["plan"], 2),
+        "eager_us_per_step": round(t_eager * 1e6, 2),
+        "dispatch_scatter_GBps": round(scatter_bytes / per_call_us["dispatch_scatter"] / 1e3, 1),
+        "pack_GBps": round(pack_bytes / per_call_us["pack"] / 1e3, 1) if pack_bytes else None,
+        "copy_reference_GBps": round(copy_gbps, 1),
+        "setup_s": round(setup_s, 2),
+    }
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(c, tk_all, rank, x_h, w_h, cap,
+                                           args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(c, tk_all, rank, x_h, w_h, cap, budget_s):
+    """The oracle (single-threaded C) on the same step, repeated until about
+    budget_s seconds of CPU work have been spent (at least one step)."""
+    import oracle
+    og = oracle.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+    tk_r = tk_all[rank]
+    load, _ = oracle.count(tk_all, c.E, c.R)  # the resident rows, not timed
+    parts = {"count": 0.0, "plan": 0.0, "dispatch": 0.0, "pack": 0.0}
+    n = 0
+    t_all = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        row, _ = oracle.count(tk_r, c.E)
+        t1 = time.perf_counter()
+        load[rank] = row[0]
+        p = oracle.plan(load, og)
+        t2 = time.perf_counter()
+        _, _, _, st = oracle.dispatch(x_h, tk_r, rank, og, p)
+        t3 = time.perf_counter()
+        _, _, _, st2 = oracle.pack(w_h, rank, og, p, cap)
+        t4 = time.perf_counter()
+        assert st == 0 and st2 == 0
+        for key, dt in zip(parts, (t1 - t0, t2 - t1, t3 - t2, t4 - t3)):
+            parts[key] += dt
+        n += 1
+        if time.perf_counter() - t_all >= budget_s:
+            break
+    tot = sum(parts.values())
+    return {
+        "value": round(tot / n * 1e6, 1),
+        "unit": "µs",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{n} full steps of the same workload and rank (count, plan, "
+                   f"dispatch with row copies, pack with blob copies), "
+                   f"{tot:.1f} s of single-threaded C on {os.cpu_count()} host cores"),
+        "parts_us": {kk: round(v / n * 1e6, 1) for kk, v in parts.items()},
+    }
+
+
+if __name__ == "__main__":
+    main()
