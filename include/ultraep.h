@@ -128,9 +128,17 @@ int ultraep_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
  * in ascending rank order, by largest remainder against the quotas still
  * unconsumed (ties to the earlier host), which keeps both margins of Q
  * exact.  Every output buffer is fully written (padding included).  Data
- * errors (negative loads, L > 2^30) set stats[6] = ULTRAEP_EDATA. */
+ * errors (negative loads, L > 2^30) set stats[6] = ULTRAEP_EDATA.
+ *   ws  device workspace of ws_bytes >= ultraep_plan_ws_bytes(g); its
+ *       contents on entry do not matter. */
 int ultraep_plan(const int32_t *load, const ultraep_group *g,
-                 const ultraep_plan_buf *out, hipStream_t stream);
+                 const ultraep_plan_buf *out, void *ws, size_t ws_bytes,
+                 hipStream_t stream);
+
+/* Bytes of device workspace ultraep_plan needs for group *g (host only; 0
+ * for an unsupported group): per-expert orders and the outcome and transfer
+ * record of every speculatively evaluated bisection probe. */
+size_t ultraep_plan_ws_bytes(const ultraep_group *g);
 
 /* Bytes of device workspace ultraep_dispatch / ultraep_dispatch_layout need
  * (host only; 0 for unsupported arguments). */

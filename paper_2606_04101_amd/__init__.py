@@ -77,7 +77,9 @@ def lib():
         gp, pp = ctypes.POINTER(Group), ctypes.POINTER(PlanBuf)
         L.ultraep_plan_sizes.argtypes = [gp, ctypes.POINTER(sz)]
         L.ultraep_count.argtypes = [_P, i64, i32, i32, i32, _P, _P, _P]
-        L.ultraep_plan.argtypes = [_P, gp, pp, _P]
+        L.ultraep_plan.argtypes = [_P, gp, pp, _P, sz, _P]
+        L.ultraep_plan_ws_bytes.argtypes = [gp]
+        L.ultraep_plan_ws_bytes.restype = sz
         L.ultraep_dispatch_ws_bytes.argtypes = [i64, i32, gp]
         L.ultraep_dispatch_ws_bytes.restype = sz
         L.ultraep_dispatch.argtypes = [_P, _P, i64, i32, i32, i32, gp, pp, _P,
@@ -132,7 +134,8 @@ def ultraep_plan_sizes(g: Group):
 
 
 class Plan:
-    """Device buffers of one plan (torch tensors) and their C descriptor."""
+    """Device buffers of one plan (torch tensors), their C descriptor, and the
+    planner's device workspace."""
 
     def __init__(self, g: Group, device="cuda"):
         import torch
@@ -142,6 +145,8 @@ class Plan:
             setattr(self, name, torch.empty(cnt, dtype=d, device=device))
         self.g = g
         self.c = PlanBuf(*[_ptr(getattr(self, f)) for f in PLAN_FIELDS])
+        self.ws = torch.empty(ultraep_plan_ws_bytes(g), dtype=torch.uint8,
+                              device=device)
 
 
 def ultraep_count(topk, T, k, E, n_groups, counts, status, stream=None):
@@ -150,10 +155,17 @@ def ultraep_count(topk, T, k, E, n_groups, counts, status, stream=None):
                                       _stream(stream)), "ultraep_count")
 
 
-def ultraep_plan(load, g: Group, plan: Plan, stream=None):
+def ultraep_plan_ws_bytes(g: Group) -> int:
+    return int(lib().ultraep_plan_ws_bytes(ctypes.byref(g)))
+
+
+def ultraep_plan(load, g: Group, plan: Plan, ws=None, stream=None):
+    """ws: device workspace (defaults to the one the Plan object holds)."""
+    ws = plan.ws if ws is None else ws
     return _check(lib().ultraep_plan(_ptr(load), ctypes.byref(g),
-                                     ctypes.byref(plan.c), _stream(stream)),
-                  "ultraep_plan")
+                                     ctypes.byref(plan.c), _ptr(ws),
+                                     ws.numel() * ws.element_size(),
+                                     _stream(stream)), "ultraep_plan")
 
 
 def ultraep_dispatch_ws_bytes(T, k, g: Group) -> int:

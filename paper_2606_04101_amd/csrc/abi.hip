@@ -59,10 +59,17 @@ int ultraep_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
   return rc(uep::launch_count(topk, T, k, E, n_groups, counts, status, stream));
 }
 
+size_t ultraep_plan_ws_bytes(const ultraep_group *g) {
+  if (!group_ok(g)) return 0;
+  return uep::plan_ws_bytes(g->R, g->E, g->n_slot);
+}
+
 int ultraep_plan(const int32_t *load, const ultraep_group *g,
-                 const ultraep_plan_buf *out, hipStream_t stream) {
-  if (!load || !group_ok(g) || !plan_ok(g, out)) return ULTRAEP_EINVAL;
-  return rc(uep::launch_plan(load, *g, *out, stream));
+                 const ultraep_plan_buf *out, void *ws, size_t ws_bytes,
+                 hipStream_t stream) {
+  if (!load || !group_ok(g) || !plan_ok(g, out) || !ws) return ULTRAEP_EINVAL;
+  if (ws_bytes < uep::plan_ws_bytes(g->R, g->E, g->n_slot)) return ULTRAEP_EINVAL;
+  return rc(uep::launch_plan(load, *g, *out, ws, stream));
 }
 
 size_t ultraep_dispatch_ws_bytes(int64_t T, int32_t k, const ultraep_group *g) {

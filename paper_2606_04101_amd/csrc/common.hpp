@@ -13,6 +13,7 @@ constexpr int kWave = 64;
 
 // 16-byte vector moved by one lane (global_load/store_dwordx4)
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ int lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0));
@@ -40,10 +41,12 @@ __device__ __forceinline__ int row_max(int v) {
   return v;
 }
 
+// Results are wave-uniform; readfirstlane makes that visible to the compiler
+// so the branches that depend on them stay scalar.
 __device__ __forceinline__ int wave_max(int v) {
   v = row_max(v);
   int a = readlane(v, 0), b = readlane(v, 16), c = readlane(v, 32), d = readlane(v, 48);
-  return max(max(a, b), max(c, d));
+  return __builtin_amdgcn_readfirstlane(max(max(a, b), max(c, d)));
 }
 
 __device__ __forceinline__ int row_sum(int v) {
@@ -56,7 +59,8 @@ __device__ __forceinline__ int row_sum(int v) {
 
 __device__ __forceinline__ int wave_sum(int v) {
   v = row_sum(v);
-  return readlane(v, 0) + readlane(v, 16) + readlane(v, 32) + readlane(v, 48);
+  return __builtin_amdgcn_readfirstlane(readlane(v, 0) + readlane(v, 16) +
+                                        readlane(v, 32) + readlane(v, 48));
 }
 
 __device__ __forceinline__ int64_t wave_sum64(int64_t v) {

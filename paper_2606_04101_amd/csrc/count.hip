@@ -1,12 +1,14 @@
 // Step 1 — exact per-expert loads lambda_{r,e} from top-k routing ids
 // (Table 1; gathered after gating in the forward pipeline of Sec. 4.2).
 //
-// One workgroup of 1024 threads per block of T*k ids.  Each wave keeps a
-// private LDS histogram; a wave aggregates equal ids with a ballot match
-// (log2(E) ballots), so one leader lane adds the whole group with a single
-// LDS update and hot experts never serialise on one bank.  The wave
-// histograms are summed at the end and every count is written (no global
-// atomics, hence no zero-fill and no memset).
+// One workgroup of 1024 threads per block of T*k ids.  Every thread issues
+// all of its 16-byte loads of a batch before using any (one memory latency
+// per batch instead of one per id), then adds each id into its wave's
+// private LDS histogram with an LDS atomic: a histogram needs no order, so
+// the per-wave privatisation bounds contention to the 64 lanes of one wave
+// (at most k lanes per token share a hot expert).  The 16 wave histograms
+// are summed at the end and every count is written (no global atomics, no
+// zero-fill, no memset).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -14,9 +16,15 @@ namespace uep {
 
 constexpr int kCountThreads = 1024;
 constexpr int kCountWaves = kCountThreads / kWave;
+constexpr int kCountBatch = 8;  // int4 loads in flight per thread
+
+__device__ __forceinline__ bool count_one(int32_t e, int32_t E, int32_t *wh) {
+  if (e >= 0 && e < E) atomicAdd(wh + e, 1);
+  return e < -1 || e >= E;
+}
 
 __global__ void __launch_bounds__(kCountThreads)
-k_count(const int32_t *__restrict__ topk, int64_t V, int32_t E, int nbits,
+k_count(const int32_t *__restrict__ topk, int64_t V, int32_t E,
         int32_t *__restrict__ counts, int32_t *status) {
   extern __shared__ int32_t hist[];  // [kCountWaves][E]
   const int wave = threadIdx.x / kWave;
@@ -26,15 +34,28 @@ k_count(const int32_t *__restrict__ topk, int64_t V, int32_t E, int nbits,
   const int32_t *src = topk + static_cast<int64_t>(blockIdx.x) * V;
   int32_t *wh = hist + wave * E;
   bool bad = false;
-  for (int64_t base = 0; base < V; base += kCountThreads) {
-    const int64_t i = base + threadIdx.x;
-    const int32_t e = i < V ? __builtin_nontemporal_load(src + i) : -1;
-    const bool valid = e >= 0 && e < E;
-    bad |= (i < V) && (e < -1 || e >= E);
-    const uint64_t act = ballot(valid);
-    if (act == 0) continue;  // wave-uniform
-    const uint64_t m = match_any(static_cast<uint32_t>(valid ? e : 0), nbits, act);
-    if (valid && popc_below(m) == 0) wh[e] += __popcll(m);
+  // the block's rows are 4-aligned only if V is: otherwise use scalar loads
+  const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(src) & 15u) == 0);
+  if (vec) {
+    const v4i *s4 = reinterpret_cast<const v4i *>(src);
+    const int64_t n4 = V / 4;
+    for (int64_t b = 0; b < n4; b += int64_t(kCountThreads) * kCountBatch) {
+      v4i v[kCountBatch];
+#pragma unroll
+      for (int u = 0; u < kCountBatch; ++u) {
+        const int64_t i = b + u * kCountThreads + threadIdx.x;
+        v[u] = i < n4 ? __builtin_nontemporal_load(s4 + i) : v4i{-1, -1, -1, -1};
+      }
+#pragma unroll
+      for (int u = 0; u < kCountBatch; ++u) {
+        bad |= count_one(v[u].x, E, wh);
+        bad |= count_one(v[u].y, E, wh);
+        bad |= count_one(v[u].z, E, wh);
+        bad |= count_one(v[u].w, E, wh);
+      }
+    }
+  } else {
+    for (int64_t i = threadIdx.x; i < V; i += kCountThreads) bad |= count_one(src[i], E, wh);
   }
   if (bad) report(status, ULTRAEP_EDATA);
   __syncthreads();
@@ -52,7 +73,7 @@ hipError_t launch_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
                         hipStream_t stream) {
   const size_t lds = sizeof(int32_t) * kCountWaves * E;
   hipLaunchKernelGGL(k_count, dim3(n_groups), dim3(kCountThreads), lds, stream,
-                     topk, T * k, E, bits_for(E), counts, status);
+                     topk, T * k, E, counts, status);
   return hipGetLastError();
 }
 

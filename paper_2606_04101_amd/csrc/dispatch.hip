@@ -27,6 +27,7 @@ constexpr int kSlotsPerWave = kDispatchChunk / kDlWaves;  // 128
 constexpr int kMaxBlocks = 2048;                           // R * S
 
 static_assert(kSlotsPerWave % kWave == 0, "chunk must split into wave steps");
+constexpr int kSteps = kSlotsPerWave / kWave;  // 64-slot steps per wave
 
 size_t dispatch_ws_bytes(int64_t V, int32_t E, int32_t ncol) {
   const int64_t n_chunks = (V + kDispatchChunk - 1) / kDispatchChunk;
@@ -52,6 +53,7 @@ struct DlArgs {
   const int32_t *topk;
   int64_t V;
   int32_t rank, R, E, NS, nm, S, ncol, nbits;
+  int32_t stage_lut;  // copy host_ptr / entry tables into LDS
   const int32_t *hp, *hr, *hs, *q;  // q = reroute row of `rank`
   int32_t *row_of_slot;
   int64_t *block_off;
@@ -70,15 +72,17 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_hist(DlArgs a) {
     const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kDispatchChunk;
     int32_t *wh = hist + wave * E;
     bool bad = false;
-    for (int s = 0; s < kSlotsPerWave; s += kWave) {
-      const int64_t i = c0 + wave * kSlotsPerWave + s + lane;
-      const int32_t e = i < a.V ? a.topk[i] : -1;
-      const bool valid = e >= 0 && e < E;
-      bad |= (i < a.V) && (e < -1 || e >= E);
-      const uint64_t act = ballot(valid);
-      if (act == 0) continue;
-      const uint64_t m = match_any(static_cast<uint32_t>(valid ? e : 0), a.nbits, act);
-      if (valid && popc_below(m) == 0) wh[e] += __popcll(m);
+    int32_t ev[kSteps];
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+      const int64_t i = c0 + wave * kSlotsPerWave + s * kWave + lane;
+      ev[s] = i < a.V ? a.topk[i] : -1;
+    }
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+      const int32_t e = ev[s];
+      if (e >= 0 && e < E) atomicAdd(wh + e, 1);
+      bad |= e < -1 || e >= E;
     }
     if (bad) report(a.status, ULTRAEP_EDATA);
     __syncthreads();
@@ -155,29 +159,52 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_rows(DlArgs a) {
   const int c = blockIdx.x;
   int32_t *whist = lds;  // [kDlWaves][E]
   int32_t *base = lds + kDlWaves * E;
-  for (int e = tid; e < E; e += kDlThreads) {
-    int s = 0;
-    for (int cc = 0; cc < c; ++cc) s += a.ws.hist[cc * static_cast<int64_t>(E) + e];
-    base[e] = s;
-    if (c == 0) {
-      int tot = 0;
-      for (int cc = 0; cc < a.ws.n_chunks; ++cc) tot += a.ws.hist[cc * static_cast<int64_t>(E) + e];
-      if (tot != a.ws.exp_tot[e]) report(a.status, ULTRAEP_EDATA);
+  // instance lookup tables, staged in LDS when they fit
+  const int32_t *l_hp = a.hp, *l_cum = a.ws.ent_cum, *l_base = a.ws.ent_base;
+  if (a.stage_lut) {
+    int32_t *p = base + E;
+    for (int i = tid; i <= E; i += kDlThreads) p[i] = a.hp[i];
+    for (int i = tid; i < a.ncol; i += kDlThreads) {
+      p[E + 1 + i] = a.ws.ent_cum[i];
+      p[E + 1 + a.ncol + i] = a.ws.ent_base[i];
     }
+    l_hp = p;
+    l_cum = p + E + 1;
+    l_base = p + E + 1 + a.ncol;
+  }
+  for (int e = tid; e < E; e += kDlThreads) {
+    // sums over chunk histograms with 8 independent loads in flight
+    const int32_t *h = a.ws.hist + e;
+    const int nsum = c == 0 ? static_cast<int>(a.ws.n_chunks) : c;
+    int s = 0, tot = 0;
+    for (int c0 = 0; c0 < nsum; c0 += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = c0 + u < nsum ? h[(c0 + u) * static_cast<int64_t>(E)] : 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        s += c0 + u < c ? v[u] : 0;
+        tot += v[u];
+      }
+    }
+    base[e] = s;
+    if (c == 0 && tot != a.ws.exp_tot[e]) report(a.status, ULTRAEP_EDATA);
   }
   for (int i = tid; i < kDlWaves * E; i += kDlThreads) whist[i] = 0;
-  __syncthreads();
   const int64_t s0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kSlotsPerWave;
+  int32_t ev[kSteps];
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+    const int64_t i = s0 + s * kWave + lane;
+    ev[s] = i < a.V ? a.topk[i] : -1;
+  }
+  __syncthreads();
   int32_t *wh = whist + wave * E;
   // pass 1: per-wave counts
-  for (int s = 0; s < kSlotsPerWave; s += kWave) {
-    const int64_t i = s0 + s + lane;
-    const int32_t e = i < a.V ? a.topk[i] : -1;
-    const bool valid = e >= 0 && e < E;
-    const uint64_t act = ballot(valid);
-    if (act == 0) continue;
-    const uint64_t m = match_any(static_cast<uint32_t>(valid ? e : 0), a.nbits, act);
-    if (valid && popc_below(m) == 0) wh[e] += __popcll(m);
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+    const int32_t e = ev[s];
+    if (e >= 0 && e < E) atomicAdd(wh + e, 1);
   }
   __syncthreads();
   for (int e = tid; e < E; e += kDlThreads) {
@@ -190,9 +217,9 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_rows(DlArgs a) {
   }
   __syncthreads();
   // pass 2: stable ordinals, instance lookup, rows
-  for (int s = 0; s < kSlotsPerWave; s += kWave) {
-    const int64_t i = s0 + s + lane;
-    const int32_t e = i < a.V ? a.topk[i] : -1;
+  for (int s = 0; s < kSteps; ++s) {
+    const int64_t i = s0 + s * kWave + lane;
+    const int32_t e = ev[s];
     const bool valid = e >= 0 && e < E;
     const uint64_t act = ballot(valid);
     if (act == 0) {
@@ -205,10 +232,10 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_rows(DlArgs a) {
       const int below = popc_below(m);
       const int ord = wh[e] + below;
       if (below == 0) wh[e] += __popcll(m);
-      const int j1 = a.hp[e + 1];
-      int j = a.hp[e];
-      while (j < j1 && a.ws.ent_cum[j] <= ord) ++j;
-      if (j < j1) row = a.ws.ent_base[j] + ord;
+      const int j1 = l_hp[e + 1];
+      int j = l_hp[e];
+      while (j < j1 && l_cum[j] <= ord) ++j;
+      if (j < j1) row = l_base[j] + ord;
       // a plan row that does not match these ids can point past the buffer
       if (row < 0 || row >= a.V) {
         row = -1;
@@ -244,14 +271,20 @@ hipError_t launch_dispatch_layout(const int32_t *topk, int64_t V, int32_t rank,
   a.block_off = block_off;
   a.ws = ws;
   a.status = status;
+  a.stage_lut = 0;
   const size_t lds_hist = sizeof(int32_t) * kDlWaves * g.E;
   const size_t lds_lay = sizeof(int32_t) * (kMaxBlocks + kDlWaves + 1);
   hipLaunchKernelGGL(k_dl_hist, dim3(ws.n_chunks + 1), dim3(kDlThreads),
                      lds_hist > lds_lay ? lds_hist : lds_lay, stream, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || ws.n_chunks == 0) return err;
-  hipLaunchKernelGGL(k_dl_rows, dim3(ws.n_chunks), dim3(kDlThreads),
-                     sizeof(int32_t) * (kDlWaves + 1) * g.E, stream, a);
+  size_t lds_rows = sizeof(int32_t) * (kDlWaves + 1) * g.E;
+  const size_t lut = sizeof(int32_t) * (g.E + 1 + 2 * static_cast<size_t>(a.ncol));
+  if (lds_rows + lut <= 64 * 1024) {
+    lds_rows += lut;
+    a.stage_lut = 1;
+  }
+  hipLaunchKernelGGL(k_dl_rows, dim3(ws.n_chunks), dim3(kDlThreads), lds_rows, stream, a);
   return hipGetLastError();
 }
 

@@ -2,36 +2,85 @@
 // threshold bisection with greedy feasibility probes of Sec. 5.1) and
 // SolveReroute (locality-first proportional split of Sec. 5.2).
 //
-// k_plan_solve: ONE workgroup of 1024 threads (16 wave64s) on one CU.
-//   - lambda_e, ell_r, the rank visiting order (descending excess is
-//     descending ell for every threshold) and each rank's expert order
-//     (descending lambda_e) are computed once and kept in LDS.
-//   - Feasibility is not monotone in tau (the u_min floor), so the probes
-//     must be exactly those of the printed sequential bisection.  Each round
-//     evaluates the whole depth-4 subtree of the bisection below the current
-//     [lo, hi): 15 probes, one per wave.  One thread then walks the subtree
-//     with the 15 outcomes, which reproduces the sequential probe sequence,
-//     and keeps the transfer record of the last feasible probe.
-//   - In a probe, lane t holds rank t's slack and used-slot count; the
-//     target of largest slack is a DPP wave max plus a ballot for the lowest
-//     rank among ties, and all control values stay wave-uniform.
-//   - The kept record is materialised into X, U and the CSR host lists.
-// k_plan_reroute: one wave per expert; lanes are sources for the locality
-//   pass and hosts for the proportional split, which walks the sources in
-//   ascending rank order (largest remainder against the residual quotas).
+// Feasibility is not monotone in tau (the u_min floor), so the probes must be
+// exactly those of the printed sequential bisection.  They are evaluated
+// speculatively across the whole chip:
+//   k_plan_prep   one workgroup: lambda_e, ell_r, the rank visiting order
+//                 (descending excess at any threshold is descending ell), each
+//                 rank's experts by descending load, tau_lo0 and tau_hi0.
+//   k_plan_round  x3 launches of 1023 one-wave workgroups.  Each workgroup
+//                 replays the walk of the earlier rounds from their stored
+//                 outcomes, then runs the probe of its node of the next depth-10
+//                 subtree of the bisection (one probe per wave on its own SIMD,
+//                 so the 1023 probes of a round run at single-probe latency).
+//                 Three depth-10 rounds cover any range below 2^30.  In a probe
+//                 lane t holds rank t's slack and slot count; the target of
+//                 largest slack (ties: lower rank) is one DPP wave max over a
+//                 packed (slack, rank) key; the accepted transfers are kept in
+//                 LDS and stored once at the end if the probe is feasible.
+//   k_plan_finish one wave per expert: walks all rounds to tau* and the last
+//                 feasible probe, materialises that probe's record into its
+//                 expert's row of U, its CSR host list, its rank's row of X, and
+//                 then splits the expert's load over its hosts (locality first,
+//                 then sources in ascending rank order by largest remainder
+//                 against the residual quotas).
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace uep {
 
-constexpr int kPlanThreads = 1024;
-constexpr int kPlanWaves = kPlanThreads / kWave;
-constexpr int kSpecNodes = 15;  // depth-4 bisection subtree per round
-constexpr int kSpecDepth = 4;
 constexpr int kMaxE = 1024;
 constexpr int kMaxR = 64;
-constexpr int kMaxRec = 256;  // R * n_slot: at most one transfer per slot
+constexpr int kMaxRec = 256;               // R * n_slot: one transfer per slot at most
+constexpr int kDepth = 10;                 // bisection levels per round
+constexpr int kNodes = (1 << kDepth) - 1;  // probes per round
+constexpr int kRounds = 3;                 // 30 levels
 constexpr int64_t kMaxLoad = int64_t(1) << 30;
+constexpr int kNotReached = INT32_MIN;
+constexpr int kPrepThreads = 1024;
+constexpr int kHdr = 4 + 4 * kRounds;  // int64 header words
+
+struct PlanWs {
+  int64_t *hdr;        // [4] tau_lo0, tau_hi0, L, status, then per round j the
+                       // bisection state after rounds 0..j: lo, hi, best, probes
+  int32_t *ell;        // [R]
+  int32_t *rank_desc;  // [R] ranks by descending load (visiting order)
+  int32_t *rank_asc;   // [R] ranks by ascending load (target order)
+  int32_t *eorder;     // [E] experts of each rank, descending load
+  int32_t *elam;       // [E] their loads
+  int32_t *lam;        // [E] lambda_e
+  int32_t *res;        // [kRounds][kNodes] probe outcome
+  uint32_t *rec;       // [kRounds][kNodes][2 * RS] (e | t << 16, delta) pairs
+};
+
+size_t plan_ws_bytes(int32_t R, int32_t E, int32_t NS) {
+  const int64_t RS = static_cast<int64_t>(R) * NS;
+  const int64_t ints = 3 * R + 3 * E + int64_t(kRounds) * kNodes * (1 + 2 * RS);
+  return static_cast<size_t>(kHdr * 8 + (ints * 4 + 255) / 256 * 256);
+}
+
+static PlanWs carve(void *ws, int32_t R, int32_t E, int32_t NS) {
+  (void)NS;
+  PlanWs w;
+  w.hdr = static_cast<int64_t *>(ws);
+  int32_t *p = reinterpret_cast<int32_t *>(w.hdr + kHdr);
+  w.ell = p;
+  p += R;
+  w.rank_desc = p;
+  p += R;
+  w.rank_asc = p;
+  p += R;
+  w.eorder = p;
+  p += E;
+  w.elam = p;
+  p += E;
+  w.lam = p;
+  p += E;
+  w.res = p;
+  p += kRounds * kNodes;
+  w.rec = reinterpret_cast<uint32_t *>(p);
+  return w;
+}
 
 struct PlanArgs {
   const int32_t *load;
@@ -40,359 +89,591 @@ struct PlanArgs {
   int64_t beta_num, beta_den;
   int32_t *X, *U, *hp, *hr, *hs, *q;
   int64_t *stats;
+  PlanWs ws;
 };
 
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-// One greedy feasibility probe at threshold tau, run by a whole wave.
-// Returns (feasible ? n : -1 - n) with n transfers recorded.
-__device__ int probe_wave(const PlanArgs &a, int tau, int lane,
-                          const int32_t *s_lam, const int32_t *s_ell,
-                          const int32_t *s_rank_desc, const int32_t *s_eorder,
-                          uint32_t *rec_et, int32_t *rec_d) {
-  int slk = lane < a.R ? max(tau - s_ell[lane], 0) : 0;
-  int used = 0;
-  int n = 0;
-  for (int oi = 0; oi < a.R; ++oi) {
-    const int r = uni(s_rank_desc[oi]);
-    int exc = uni(s_ell[r]) - tau;
-    if (exc <= 0) break;  // the remaining ranks are not overloaded
-    for (int j = 0; j < a.nm && exc > 0; ++j) {
-      const int e = uni(s_eorder[r * a.nm + j]);
-      int cap = uni(s_lam[e]);
-      while (exc > 0 && cap > 0) {
-        const int v = (slk > 0 && used < a.NS) ? slk : 0;
-        const int m = wave_max(v);
-        if (m == 0) break;  // no admissible rank
-        const int ts = uni(__ffsll(static_cast<unsigned long long>(ballot(v == m))) - 1);
-        const int d = min(min(exc, m), cap);
-        if (d < a.u_min) break;
-        if (lane == ts) {
-          slk -= d;
-          ++used;
-        }
-        if (lane == 0) {
-          rec_et[n] = static_cast<uint32_t>(e) | (static_cast<uint32_t>(ts) << 16);
-          rec_d[n] = d;
-        }
-        ++n;
-        exc -= d;
-        cap -= d;
-      }
-    }
-    if (exc > 0) return -1 - n;
-  }
-  return n;
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const long long b = __double_as_longlong(v);
+  const int lo = readlane(static_cast<int>(b), l), hi = readlane(static_cast<int>(b >> 32), l);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<uint32_t>(lo));
 }
 
-__device__ int block_exclusive_scan(int v, int *s_tmp, int *total) {
-  // s_tmp: kPlanWaves + 1 ints
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
-  int incl = v;
-  for (int o = 1; o < kWave; o <<= 1) {
-    int t = __shfl_up(incl, o);
-    if (lane >= o) incl += t;
-  }
-  if (lane == kWave - 1) s_tmp[wave] = incl;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int w = 0; w < kPlanWaves; ++w) {
-      int t = s_tmp[w];
-      s_tmp[w] = run;
-      run += t;
-    }
-    s_tmp[kPlanWaves] = run;
-  }
-  __syncthreads();
-  int ex = s_tmp[wave] + incl - v;
-  *total = s_tmp[kPlanWaves];
-  __syncthreads();
-  return ex;
-}
+// ---------------------------------------------------------------- prep
 
-__global__ void __launch_bounds__(kPlanThreads) k_plan_solve(PlanArgs a) {
+__global__ void __launch_bounds__(kPrepThreads) k_plan_prep(PlanArgs a) {
   __shared__ int32_t s_lam[kMaxE];
-  __shared__ int32_t s_eorder[kMaxE];
-  __shared__ int32_t s_fan[kMaxE];
-  __shared__ int32_t s_shed[kMaxE];
-  __shared__ int32_t s_hp[kMaxE + 1];
   __shared__ int32_t s_ell[kMaxR];
-  __shared__ int32_t s_rank_desc[kMaxR];
-  __shared__ uint32_t s_rec_et[kSpecNodes][kMaxRec];
-  __shared__ int32_t s_rec_d[kSpecNodes][kMaxRec];
-  __shared__ uint32_t s_best_et[kMaxRec];
-  __shared__ int32_t s_best_d[kMaxRec];
-  __shared__ int32_t s_X[kMaxRec];
-  __shared__ int32_t s_Xd[kMaxRec];
-  __shared__ int32_t s_res[kSpecNodes];
-  __shared__ int32_t s_tmp[kPlanWaves + 1];
-  __shared__ int64_t s_lo, s_hi, s_lo0, s_hi0;
+  __shared__ int64_t s_part[kPrepThreads];
   __shared__ unsigned long long s_L;
-  __shared__ int32_t s_bad, s_best_node, s_nbest, s_nprobe;
-
-  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  const int R = a.R, E = a.E, NS = a.NS, nm = a.nm, RS = R * NS;
-
+  __shared__ int32_t s_bad;
+  const int tid = threadIdx.x, lane = lane_id();
+  const int R = a.R, E = a.E, nm = a.nm;
   if (tid == 0) {
     s_L = 0;
     s_bad = 0;
-    s_nbest = 0;
-    s_nprobe = 0;
   }
   __syncthreads();
-
-  // lambda_e = sum_r lambda_{r,e}
-  int64_t lam = 0;
-  if (tid < E) {
-    bool neg = false;
-    for (int r = 0; r < R; ++r) {
-      int v = a.load[static_cast<int64_t>(r) * E + tid];
-      neg |= v < 0;
-      lam += v;
+  // lambda_e: thread (part, e) sums rows part, part + parts, ... with up to
+  // 16 loads in flight, the parts are then combined in LDS
+  const int parts = max(1, kPrepThreads / E);
+  const int pe = tid % E, part = tid / E;
+  int64_t psum = 0;
+  bool neg = false;
+  if (part < parts) {
+    for (int r0 = part; r0 < R; r0 += 16 * parts) {
+      int v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int r = r0 + u * parts;
+        v[u] = r < R ? a.load[static_cast<int64_t>(r) * E + pe] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        neg |= v[u] < 0;
+        psum += v[u];
+      }
     }
-    if (neg || lam > kMaxLoad) atomicOr(&s_bad, 1);
-    s_lam[tid] = static_cast<int32_t>(min(lam, kMaxLoad));
   }
+  if (neg) atomicOr(&s_bad, 1);
+  s_part[tid] = psum;
   {
-    int64_t ws = wave_sum64(lam);
-    if (lane == 0) atomicAdd(&s_L, static_cast<unsigned long long>(ws));
+    const int64_t w = wave_sum64(psum);
+    if (lane == 0) atomicAdd(&s_L, static_cast<unsigned long long>(w));
+  }
+  __syncthreads();
+  if (tid < E) {
+    int64_t lam = 0;
+    for (int p = 0; p < parts; ++p) lam += s_part[p * E + tid];
+    if (lam > kMaxLoad) atomicOr(&s_bad, 1);
+    s_lam[tid] = static_cast<int32_t>(min(lam, kMaxLoad));
+    a.ws.lam[tid] = static_cast<int32_t>(min(lam, kMaxLoad));
   }
   __syncthreads();
   const int64_t L = static_cast<int64_t>(s_L);
   if (s_bad || L > kMaxLoad) {
-    if (tid < 8) a.stats[tid] = tid == 6 ? ULTRAEP_EDATA : (tid == 7 ? L : 0);
+    if (tid == 0) {
+      a.ws.hdr[2] = L;
+      a.ws.hdr[3] = ULTRAEP_EDATA;
+    }
     return;
   }
-  // ell_r = sum of the loads of rank r's main experts
   if (tid < R) {
     int s = 0;
     for (int j = 0; j < nm; ++j) s += s_lam[tid * nm + j];
     s_ell[tid] = s;
+    a.ws.ell[tid] = s;
   }
-  // each rank's main experts by descending load (ties: lower id)
-  if (tid < E) {
+  if (tid < E) {  // each rank's main experts by descending load (ties: lower id)
     const int r = tid / nm, l = s_lam[tid];
     int pos = 0;
     for (int j = r * nm; j < r * nm + nm; ++j) {
-      int lj = s_lam[j];
+      const int lj = s_lam[j];
       pos += (lj > l) || (lj == l && j < tid);
     }
-    s_eorder[r * nm + pos] = tid;
+    a.ws.eorder[r * nm + pos] = tid;
+    a.ws.elam[r * nm + pos] = l;
   }
   __syncthreads();
-  // ranks by descending load = descending excess at any threshold
-  if (tid < R) {
-    const int l = s_ell[tid];
-    int pos = 0;
-    for (int r = 0; r < R; ++r) {
-      int lr = s_ell[r];
-      pos += (lr > l) || (lr == l && r < tid);
-    }
-    s_rank_desc[pos] = tid;
-  }
-  if (tid == 0) {
-    const int64_t m = (L + R - 1) / R;
-    const int64_t lo = (a.beta_num * m + a.beta_den - 1) / a.beta_den;
-    int64_t hi = 0;
-    for (int r = 0; r < R; ++r) hi = max(hi, static_cast<int64_t>(s_ell[r]));
-    s_lo = s_lo0 = lo;
-    s_hi = s_hi0 = hi;
-  }
-
-  // ---- SolveReplication: speculative exact bisection -------------------
-  for (;;) {
-    __syncthreads();
-    const int64_t lo = s_lo, hi = s_hi;
-    if (lo >= hi) break;
-    if (wave < kSpecNodes) {
-      const int id = wave + 1;
-      const int depth = 31 - __clz(id);
-      int64_t l = lo, h = hi;
-      bool ok = true;
-      for (int b = depth - 1; b >= 0; --b) {
-        if (l >= h) {
-          ok = false;
-          break;
-        }
-        const int64_t mid = (l + h) / 2;
-        if ((id >> b) & 1) l = mid + 1;  // right child: the probe failed
-        else h = mid;                    // left child: the probe succeeded
+  if (tid < kWave) {  // ranks by descending load (ties: lower rank); R <= 64
+    const int l = tid < R ? s_ell[tid] : -1;
+    if (tid < R) {
+      int pos = 0;
+      for (int r = 0; r < R; ++r) {
+        const int lr = s_ell[r];
+        pos += (lr > l) || (lr == l && r < tid);
       }
-      int res = INT32_MIN;  // node not reached
-      if (ok && l < h)
-        res = probe_wave(a, static_cast<int>((l + h) / 2), lane, s_lam, s_ell,
-                         s_rank_desc, s_eorder, s_rec_et[wave], s_rec_d[wave]);
-      if (lane == 0) s_res[wave] = res;
+      a.ws.rank_desc[pos] = tid;
+      int apos = 0;  // ascending load, ties: lower rank
+      for (int r = 0; r < R; ++r) {
+        const int lr = s_ell[r];
+        apos += (lr < l) || (lr == l && r < tid);
+      }
+      a.ws.rank_asc[apos] = tid;
     }
-    __syncthreads();
+    const int hi = wave_max(l);
     if (tid == 0) {
-      int64_t l = lo, h = hi;
-      int node = 0, best = -1, np = 0;
-      for (int d = 0; d < kSpecDepth && l < h; ++d) {
-        const int64_t mid = (l + h) / 2;
-        ++np;
-        if (s_res[node] >= 0) {
-          h = mid;
-          best = node;
-          node = 2 * node + 1;
-        } else {
-          l = mid + 1;
-          node = 2 * node + 2;
-        }
-      }
-      s_lo = l;
-      s_hi = h;
-      s_nprobe += np;
-      s_best_node = best;
-      if (best >= 0) s_nbest = s_res[best];
+      const int64_t m = (L + R - 1) / R;
+      const int64_t lo = (a.beta_num * m + a.beta_den - 1) / a.beta_den;
+      a.ws.hdr[0] = lo;
+      a.ws.hdr[1] = hi;
+      a.ws.hdr[2] = L;
+      a.ws.hdr[3] = 0;
     }
-    __syncthreads();
-    const int best = s_best_node;
-    if (best >= 0)
-      for (int i = tid; i < s_nbest; i += kPlanThreads) {
-        s_best_et[i] = s_rec_et[best][i];
-        s_best_d[i] = s_rec_d[best][i];
-      }
-  }
-
-  // ---- materialise X, U and the host lists ------------------------------
-  const int nb = s_nbest;  // zero when no probe succeeded: identity plan
-  for (int i = tid; i < RS; i += kPlanThreads) {
-    s_X[i] = -1;
-    s_Xd[i] = 0;
-  }
-  __syncthreads();
-  if (tid < nb) {
-    const uint32_t et = s_best_et[tid];
-    const int t = static_cast<int>(et >> 16);
-    int slot = 0;
-    for (int j = 0; j < tid; ++j) slot += static_cast<int>(s_best_et[j] >> 16) == t;
-    s_X[t * NS + slot] = static_cast<int>(et & 0xFFFFu);
-    s_Xd[t * NS + slot] = s_best_d[tid];
-  }
-  __syncthreads();
-  for (int i = tid; i < RS; i += kPlanThreads) a.X[i] = s_X[i];
-  int fan = 0;
-  if (tid < E) {
-    int shed = 0;
-    for (int j = 0; j < RS; ++j)
-      if (s_X[j] == tid) {
-        ++fan;
-        shed += s_Xd[j];
-      }
-    s_fan[tid] = fan;
-    s_shed[tid] = shed;
-  }
-  int total;
-  const int ex = block_exclusive_scan(tid < E ? 1 + fan : 0, s_tmp, &total);
-  if (tid < E) {
-    s_hp[tid] = ex;
-    a.hp[tid] = ex;
-    const int h = tid / nm;
-    a.hr[ex] = h;
-    a.hs[ex] = tid - h * nm;
-  }
-  if (tid == 0) {
-    s_hp[E] = total;
-    a.hp[E] = total;
-  }
-  __syncthreads();
-  if (tid < RS && s_X[tid] >= 0) {
-    const int e = s_X[tid], t = tid / NS, s = tid - t * NS;
-    int pos = 1;
-    for (int j = 0; j < t * NS; ++j) pos += s_X[j] == e;
-    const int ent = s_hp[e] + pos;
-    a.hr[ent] = t;
-    a.hs[ent] = nm + s;
-  }
-  for (int j = total + tid; j < a.ncol; j += kPlanThreads) {
-    a.hr[j] = -1;
-    a.hs[j] = -1;
-  }
-  for (int i = tid; i < E * R; i += kPlanThreads) {
-    const int e = i / R, t = i - e * R;
-    int v = 0;
-    if (t == e / nm) {
-      v = s_lam[e] - s_shed[e];
-    } else {
-      for (int s = 0; s < NS; ++s)
-        if (s_X[t * NS + s] == e) v = s_Xd[t * NS + s];
-    }
-    a.U[i] = v;
-  }
-  // stats
-  int maxh = 0;
-  if (tid < E) maxh = 1 + s_fan[tid];
-  maxh = wave_max(maxh);
-  if (lane == 0) s_tmp[wave] = maxh;
-  __syncthreads();
-  if (tid == 0) {
-    int mh = 0;
-    for (int w = 0; w < kPlanWaves; ++w) mh = max(mh, s_tmp[w]);
-    a.stats[0] = s_hi;
-    a.stats[1] = s_lo0;
-    a.stats[2] = s_hi0;
-    a.stats[3] = s_nprobe;
-    a.stats[4] = nb;
-    a.stats[5] = mh;
-    a.stats[6] = 0;
-    a.stats[7] = L;
   }
 }
 
-// ---- SolveReroute: one wave per expert ---------------------------------
-__global__ void __launch_bounds__(kWave) k_plan_reroute(PlanArgs a) {
-  const int e = blockIdx.x, lane = threadIdx.x;
-  const int R = a.R, E = a.E, ncol = a.ncol;
-  if (a.stats[6] != 0) return;
-  const int j0 = a.hp[e], nh = a.hp[e + 1] - j0, total = a.hp[E];
-  // zero the CSR padding columns (spread over the expert blocks)
-  for (int j = total + e; j < ncol; j += E)
-    for (int r = lane; r < R; r += kWave) a.q[static_cast<int64_t>(r) * ncol + j] = 0;
+// ---------------------------------------------------------------- rounds
 
-  const int lam_r = lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
-  if (nh == 1) {
-    if (lane < R) a.q[static_cast<int64_t>(lane) * ncol + j0] = lam_r;
+// Walks the depth-kDepth subtree of one round over its stored outcomes
+// (s_res), from [lo, hi): updates the interval, the last feasible node and
+// the number of probes of the sequential bisection.
+__device__ void walk_round(const int32_t *s_res, int64_t &lo, int64_t &hi, int &best,
+                           int &n_probe) {
+  int node = 0;
+  for (int d = 0; d < kDepth && lo < hi; ++d) {
+    const int64_t mid = (lo + hi) / 2;
+    ++n_probe;
+    if (uni(s_res[node]) >= 0) {
+      hi = mid;
+      best = node;
+      node = 2 * node + 1;
+    } else {
+      lo = mid + 1;
+      node = 2 * node + 2;
+    }
+  }
+}
+
+// All kNodes outcomes of one round into LDS: 16 independent loads per lane.
+__device__ void load_round(const int32_t *res, int32_t *s_res, int lane) {
+  int v[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int i = u * kWave + lane;
+    v[u] = i < kNodes ? __builtin_nontemporal_load(res + i) : 0;
+  }
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int i = u * kWave + lane;
+    if (i < kNodes) s_res[i] = v[u];
+  }
+}
+
+// DPP wave_shl:1 - lane i receives lane i+1 (lane 63 keeps its value)
+__device__ __forceinline__ int wave_shl1(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x130, 0xF, 0xF, false);
+}
+
+// One greedy feasibility probe at threshold tau, run by one wave.  Lane i
+// holds the i-th rank of the visiting order (rk_r) and its load (rk_l).
+// Returns the number of transfers if feasible, else a negative value.
+//
+// Admissible targets (slack > 0, a free slot) are kept as a list sorted by
+// (slack descending, rank ascending) across the lanes from the head `h`
+// on, each as a packed key (slack << 6) | (63 - rank) (slacks < 2^25) with
+// its used-slot count beside it.  The list starts as the ranks in ascending
+// load order (the same order at every threshold) cut at load < tau.  A
+// transfer reads the head; a target whose slack or slots run out leaves the
+// list by advancing h, otherwise it moves back to its place in the order.
+__device__ int probe_sorted(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
+                            int as_r, int as_l, const int32_t *s_eorder,
+                            const int32_t *s_elam, uint32_t *s_re, int32_t *s_rd) {
+  int key = (lane < a.R && as_l < tau && a.NS > 0) ? ((tau - as_l) << 6) | (kWave - 1 - as_r) : 0;
+  int used = 0;
+  int h = 0;
+  int n = 0;
+  for (int oi = 0; oi < a.R; ++oi) {
+    int exc = readlane(rk_l, oi) - tau;
+    if (exc <= 0) break;  // the remaining ranks are not overloaded
+    const int r = readlane(rk_r, oi);
+    for (int j0 = 0; j0 < a.nm && exc > 0; j0 += kWave) {
+      const int jl = j0 + lane;
+      const int ev = jl < a.nm ? s_eorder[r * a.nm + jl] : 0;
+      const int lv = jl < a.nm ? s_elam[r * a.nm + jl] : 0;
+      const int jn = min(kWave, a.nm - j0);
+      for (int j = 0; j < jn && exc > 0; ++j) {
+        const int e = readlane(ev, j);
+        int cap = readlane(lv, j);
+        while (exc > 0 && cap > 0) {
+          // no admissible rank: the same holds for every later expert of r
+          if (h >= kWave) return -1;
+          const int kh = readlane(key, h);
+          if (kh == 0) return -1;
+          const int m = kh >> 6;
+          const int d = min(min(exc, m), cap);
+          if (d < a.u_min) {
+            // bounded by the excess or the slack: every later expert of r
+            // meets the same bound, so r keeps its excess
+            if (min(exc, m) < a.u_min) return -1;
+            break;  // bounded by this expert's remaining load: next expert
+          }
+          const int ts = kWave - 1 - (kh & (kWave - 1));
+          const int uh = readlane(used, h) + 1;
+          if (m == d || uh >= a.NS) {
+            ++h;  // out of slack or slots
+          } else {
+            const int nk = ((m - d) << 6) | (kh & (kWave - 1));
+            // new place p: after every listed key still larger than nk
+            const int p = h + __popcll(ballot(lane > h && key > nk));
+            const int ks = wave_shl1(key), us = wave_shl1(used);
+            const bool mv = lane >= h && lane < p;
+            key = mv ? ks : (lane == p ? nk : key);
+            used = mv ? us : (lane == p ? uh : used);
+          }
+          if (lane == 0) {
+            s_re[n] = static_cast<uint32_t>(e) | (static_cast<uint32_t>(ts) << 16);
+            s_rd[n] = d;
+          }
+          ++n;
+          exc -= d;
+          cap -= d;
+        }
+      }
+    }
+    if (exc > 0) return -1;
+  }
+  return n;
+}
+
+// The same probe for slacks of 25 bits or more: lane t holds rank t's slack
+// and slot count, and the target is a wave max plus a ballot for the lowest
+// rank among ties.
+__device__ int probe_wide(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
+                          int ell_lane, const int32_t *s_eorder, const int32_t *s_elam,
+                          uint32_t *s_re, int32_t *s_rd) {
+  int slk = lane < a.R ? max(tau - ell_lane, 0) : 0;
+  int used = 0;
+  int n = 0;
+  for (int oi = 0; oi < a.R; ++oi) {
+    int exc = readlane(rk_l, oi) - tau;
+    if (exc <= 0) break;
+    const int r = readlane(rk_r, oi);
+    for (int j0 = 0; j0 < a.nm && exc > 0; j0 += kWave) {
+      const int jl = j0 + lane;
+      const int ev = jl < a.nm ? s_eorder[r * a.nm + jl] : 0;
+      const int lv = jl < a.nm ? s_elam[r * a.nm + jl] : 0;
+      const int jn = min(kWave, a.nm - j0);
+      for (int j = 0; j < jn && exc > 0; ++j) {
+        const int e = readlane(ev, j);
+        int cap = readlane(lv, j);
+        while (exc > 0 && cap > 0) {
+          const bool ok = slk > 0 && used < a.NS;
+          const int v = ok ? slk : 0;
+          const int m = wave_max(v);
+          if (m == 0) return -1;
+          const int ts = uni(__ffsll(static_cast<unsigned long long>(ballot(v == m && ok))) - 1);
+          const int d = min(min(exc, m), cap);
+          if (d < a.u_min) {
+            if (min(exc, m) < a.u_min) return -1;
+            break;
+          }
+          if (lane == ts) {
+            slk -= d;
+            ++used;
+          }
+          if (lane == 0) {
+            s_re[n] = static_cast<uint32_t>(e) | (static_cast<uint32_t>(ts) << 16);
+            s_rd[n] = d;
+          }
+          ++n;
+          exc -= d;
+          cap -= d;
+        }
+      }
+    }
+    if (exc > 0) return -1;
+  }
+  return n;
+}
+
+// Bisection state after rounds 0 .. upto: the state after the round before
+// (header slot, or the initial interval), then a walk of round `upto` over
+// its stored outcomes.
+struct BisState {
+  int64_t lo, hi;
+  int best;   // last feasible probe: round * kNodes + node, or -1
+  int probes; // probes of the sequential bisection so far
+};
+
+__device__ BisState state_after(const PlanArgs &a, int upto, int32_t *s_res, int lane) {
+  BisState st;
+  if (upto == 0) {
+    st = {a.ws.hdr[0], a.ws.hdr[1], -1, 0};
+  } else {
+    const int64_t *h = a.ws.hdr + 4 + 4 * (upto - 1);
+    st = {h[0], h[1], static_cast<int>(h[2]), static_cast<int>(h[3])};
+  }
+  if (st.lo < st.hi) {
+    load_round(a.ws.res + upto * kNodes, s_res, lane);
+    __syncthreads();
+    int best = -1;
+    walk_round(s_res, st.lo, st.hi, best, st.probes);
+    if (best >= 0) st.best = upto * kNodes + best;
+  }
+  return st;
+}
+
+__global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
+  __shared__ int32_t s_res[kNodes];
+  __shared__ int32_t s_eorder[kMaxE];
+  __shared__ int32_t s_elam[kMaxE];
+  __shared__ uint32_t s_re[kMaxRec];
+  __shared__ int32_t s_rd[kMaxRec];
+  const int lane = threadIdx.x, b = blockIdx.x;
+  const int RS = a.R * a.NS;
+  if (a.ws.hdr[3] != 0) return;
+  int64_t lo, hi;
+  if (round == 0) {
+    lo = a.ws.hdr[0];
+    hi = a.ws.hdr[1];
+  } else {
+    // every workgroup walks the previous round; workgroup 0 publishes it
+    const BisState st = state_after(a, round - 1, s_res, lane);
+    if (b == 0 && lane == 0) {
+      int64_t *h = a.ws.hdr + 4 + 4 * (round - 1);
+      h[0] = st.lo;
+      h[1] = st.hi;
+      h[2] = st.best;
+      h[3] = st.probes;
+    }
+    lo = st.lo;
+    hi = st.hi;
+  }
+  if (lo >= hi) return;  // the bisection has ended
+  const bool packed = a.ws.hdr[1] < (int64_t(1) << 25);
+  // this workgroup's node of the round's subtree
+  const int id = b + 1, depth = 31 - __clz(id);
+  bool reached = true;
+  for (int bit = depth - 1; bit >= 0 && reached; --bit) {
+    const int64_t mid = (lo + hi) / 2;
+    if ((id >> bit) & 1) lo = mid + 1;  // right child: that probe failed
+    else hi = mid;                      // left child: that probe succeeded
+    reached = lo < hi;
+  }
+  int n = kNotReached;
+  if (reached) {
+    const int tau = static_cast<int>((lo + hi) / 2);
+    {  // stage the per-rank expert orders: up to 16 loads per lane in flight
+      for (int i0 = 0; i0 < a.E; i0 += 16 * kWave) {
+        int ve[16], vl[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int i = i0 + u * kWave + lane;
+          ve[u] = i < a.E ? a.ws.eorder[i] : 0;
+          vl[u] = i < a.E ? a.ws.elam[i] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int i = i0 + u * kWave + lane;
+          if (i < a.E) {
+            s_eorder[i] = ve[u];
+            s_elam[i] = vl[u];
+          }
+        }
+      }
+    }
+    const int rk_r = lane < a.R ? a.ws.rank_desc[lane] : 0;
+    const int as_r = lane < a.R ? a.ws.rank_asc[lane] : 0;
+    const int ell_lane = lane < a.R ? a.ws.ell[lane] : 0;
+    const int rk_l = __shfl(ell_lane, rk_r);
+    const int as_l = __shfl(ell_lane, as_r);
+    __syncthreads();
+    n = packed ? probe_sorted(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd)
+               : probe_wide(a, tau, lane, rk_r, rk_l, ell_lane, s_eorder, s_elam, s_re, s_rd);
+    if (n > 0) {
+      __syncthreads();
+      uint32_t *rec = a.ws.rec + (static_cast<int64_t>(round) * kNodes + b) * 2 * RS;
+      for (int i = lane; i < n; i += kWave) {
+        rec[2 * i] = s_re[i];
+        rec[2 * i + 1] = static_cast<uint32_t>(s_rd[i]);
+      }
+    }
+  }
+  if (lane == 0) a.ws.res[round * kNodes + b] = n;
+}
+
+// ---------------------------------------------------------------- finish
+
+__global__ void __launch_bounds__(kWave) k_plan_finish(PlanArgs a) {
+  __shared__ int32_t s_res[kNodes];
+  __shared__ uint32_t s_et[kMaxRec];
+  __shared__ int32_t s_d[kMaxRec];
+  __shared__ int32_t s_ht[kMaxR];  // hosts of this expert: rank
+  __shared__ int32_t s_hu[kMaxR];  //                       quota
+  __shared__ int32_t s_fan[kMaxE];
+  const int e = blockIdx.x, lane = threadIdx.x;
+  const int R = a.R, E = a.E, NS = a.NS, nm = a.nm, ncol = a.ncol, RS = R * NS;
+  if (a.ws.hdr[3] != 0) {
+    if (e == 0 && lane < 8) a.stats[lane] = lane == 6 ? ULTRAEP_EDATA : (lane == 7 ? a.ws.hdr[2] : 0);
     return;
   }
-  // locality: each source that hosts e first consumes its own quota
-  const int u_r = lane < R ? a.U[static_cast<int64_t>(e) * R + lane] : 0;
-  const int loc_r = min(lam_r, u_r);
-  const int lamhat_r = lam_r - loc_r;
-  const int t_i = lane < nh ? a.hr[j0 + lane] : 0;
-  const int u_i = lane < nh ? a.U[static_cast<int64_t>(e) * R + t_i] : 0;
-  const int qloc_i = __shfl(loc_r, t_i);
-  int ures = lane < nh ? u_i - qloc_i : 0;
-  int D = wave_sum(ures);
-  for (int r = 0; r < R; ++r) {
-    const int lh = readlane(lamhat_r, r);
-    int qi = 0;
-    if (lh > 0) {
-      const uint64_t prod = static_cast<uint64_t>(lh) * static_cast<uint64_t>(ures);
-      const int base = static_cast<int>(prod / static_cast<uint64_t>(D));
-      const int rem = static_cast<int>(prod - static_cast<uint64_t>(base) * static_cast<uint64_t>(D));
-      const int left = lh - wave_sum(base);
-      int extra = 0;
-      if (left > 0) {
-        int rk = 0;
-        for (int j = 0; j < nh; ++j) {
-          const int rj = readlane(rem, j);
-          rk += (rj > rem) || (rj == rem && j < lane);
-        }
-        extra = (lane < nh && rk < left) ? 1 : 0;
-      }
-      qi = base + extra;
-      ures -= qi;
-      D -= lh;
+  const int64_t lo0 = a.ws.hdr[0], hi0 = a.ws.hdr[1];
+  const BisState fin = state_after(a, kRounds - 1, s_res, lane);
+  const int64_t hi = fin.hi;
+  const int n_probe = fin.probes;
+  const int best = fin.best;
+  const int nb = best >= 0 ? a.ws.res[best] : 0;
+  if (best >= 0) {
+    const uint32_t *rec = a.ws.rec + static_cast<int64_t>(best) * 2 * RS;
+    for (int i = lane; i < nb; i += kWave) {
+      s_et[i] = rec[2 * i];
+      s_d[i] = static_cast<int32_t>(rec[2 * i + 1]);
     }
-    if (lane < nh)
-      a.q[static_cast<int64_t>(r) * ncol + j0 + lane] = qi + (t_i == r ? qloc_i : 0);
   }
+  __syncthreads();
+  const int h = e / nm;
+  const int lam_e = a.ws.lam[e];
+
+  // CSR row pointer: every expert has 1 + (its replicas) entries
+  int before = 0, shed = 0;
+  for (int i = lane; i < nb; i += kWave) {
+    const int ei = static_cast<int>(s_et[i] & 0xFFFFu);
+    before += ei < e;
+    if (ei == e) shed += s_d[i];
+  }
+  before = wave_sum(before);
+  shed = wave_sum(shed);
+  const int hp_e = e + before;
+  // this expert's replicas: position among them = replicas on lower ranks;
+  // slot on the host = earlier accepted transfers to the same rank
+  int fan = 0;
+  for (int i0 = 0; i0 < nb; i0 += kWave) {
+    const int i = i0 + lane;
+    const bool mine = i < nb && static_cast<int>(s_et[i] & 0xFFFFu) == e;
+    const uint64_t mb = ballot(mine);
+    if (mine) {
+      const int t = static_cast<int>(s_et[i] >> 16);
+      int pos = 0, slot = 0;
+      for (int j = 0; j < nb; ++j) {
+        const uint32_t x = s_et[j];
+        pos += static_cast<int>(x & 0xFFFFu) == e && static_cast<int>(x >> 16) < t;
+        slot += j < i && static_cast<int>(x >> 16) == t;
+      }
+      s_ht[1 + pos] = t;
+      s_hu[1 + pos] = s_d[i];
+      a.hr[hp_e + 1 + pos] = t;
+      a.hs[hp_e + 1 + pos] = nm + slot;
+    }
+    fan += __popcll(mb);
+  }
+  const int nh = 1 + fan;
+  if (lane == 0) {
+    s_ht[0] = h;
+    s_hu[0] = lam_e - shed;
+    a.hp[e] = hp_e;
+    a.hr[hp_e] = h;
+    a.hs[hp_e] = e - h * nm;
+    if (e == E - 1) a.hp[E] = E + nb;
+  }
+  for (int j = E + nb + e; j < ncol; j += E) {  // CSR padding
+    if (lane == 0) {
+      a.hr[j] = -1;
+      a.hs[j] = -1;
+    }
+  }
+  // row e of U
+  __syncthreads();
+  int u_r = 0;  // quota of this expert on rank `lane`
+  for (int i = 0; i < nh; ++i)
+    if (s_ht[i] == lane) u_r = s_hu[i];
+  if (lane < R) a.U[static_cast<int64_t>(e) * R + lane] = u_r;
+  // row t = e of X (one workgroup per rank): slots in acceptance order
+  if (e < R && NS > 0) {
+    int cnt = 0;
+    for (int i0 = 0; i0 < nb; i0 += kWave) {
+      const int i = i0 + lane;
+      const bool to_me = i < nb && static_cast<int>(s_et[i] >> 16) == e;
+      const uint64_t mb = ballot(to_me);
+      if (to_me) a.X[e * NS + cnt + popc_below(mb)] = static_cast<int>(s_et[i] & 0xFFFFu);
+      cnt += __popcll(mb);
+    }
+    for (int s = cnt + lane; s < NS; s += kWave) a.X[e * NS + s] = -1;
+  }
+  if (e == 0) {  // stats
+    for (int i = lane; i < E; i += kWave) s_fan[i] = 0;
+    __syncthreads();
+    for (int i = lane; i < nb; i += kWave) atomicAdd(&s_fan[s_et[i] & 0xFFFFu], 1);
+    __syncthreads();
+    int mf = 0;
+    for (int i = lane; i < E; i += kWave) mf = max(mf, s_fan[i]);
+    mf = wave_max(mf);
+    if (lane == 0) {
+      a.stats[0] = hi;
+      a.stats[1] = lo0;
+      a.stats[2] = hi0;
+      a.stats[3] = n_probe;
+      a.stats[4] = nb;
+      a.stats[5] = 1 + mf;
+      a.stats[6] = 0;
+      a.stats[7] = a.ws.hdr[2];
+    }
+  }
+
+  // ---- SolveReroute for expert e ------------------------------------------
+  const int lam_r = lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
+  if (nh == 1) {
+    if (lane < R) a.q[static_cast<int64_t>(lane) * ncol + hp_e] = lam_r;
+  } else {
+    // locality: a source that hosts e first consumes its own quota
+    const int loc_r = min(lam_r, u_r);
+    const int lamhat_r = lam_r - loc_r;
+    const int t_i = lane < nh ? s_ht[lane] : 0;
+    const int qloc_i = __shfl(loc_r, t_i);
+    int ures = lane < nh ? s_hu[lane] - qloc_i : 0;
+    // residual quota total seen by source r: D_0 minus the demand of the
+    // sources before it; its reciprocal, all computed lane-parallel up front
+    int incl = lamhat_r;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int t = __shfl_up(incl, o);
+      if (lane >= o) incl += t;
+    }
+    const int D0 = wave_sum(ures);
+    const int Dr = D0 - (incl - lamhat_r);
+    const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
+    const bool one_row = nh <= 16;
+    // loads below 2^26: every product below 2^52, so fp64 is exact
+    const bool exact_fp64 = a.ws.hdr[2] < (int64_t(1) << 26);
+    const int64_t col = hp_e + lane;
+    for (int r = 0; r < R; ++r) {
+      const int lh = readlane(lamhat_r, r);
+      int qi = 0;
+      if (lh > 0) {
+        const int D = readlane(Dr, r);
+        const double rD = readlane_d(rDr, r);
+        // floor(lh * ures / D): fp64 estimate (far below one unit off since
+        // the quotient is < 2^30), made exact by one correction
+        int b, rem;
+        if (exact_fp64) {
+          const double Dd = static_cast<double>(D);
+          const double pr = static_cast<double>(lh) * static_cast<double>(ures);
+          double bq = __builtin_trunc(pr * rD);
+          double rd = __builtin_fma(-bq, Dd, pr);
+          if (rd < 0.0) {
+            bq -= 1.0;
+            rd += Dd;
+          } else if (rd >= Dd) {
+            bq += 1.0;
+            rd -= Dd;
+          }
+          b = static_cast<int>(bq);
+          rem = static_cast<int>(rd);
+        } else {
+          b = static_cast<int>(static_cast<double>(lh) * static_cast<double>(ures) * rD);
+          int64_t rm = static_cast<int64_t>(lh) * ures - static_cast<int64_t>(b) * D;
+          if (rm < 0) {
+            --b;
+            rm += D;
+          } else if (rm >= D) {
+            ++b;
+            rm -= D;
+          }
+          rem = static_cast<int>(rm);
+        }
+        const int left = lh - (one_row ? readlane(row_sum(b), 0) : wave_sum(b));
+        int extra = 0;
+        if (left > 0) {  // the `left` hosts with the largest remainders
+          int rk = 0;
+          for (int j = 0; j < nh; ++j) {
+            const int rj = readlane(rem, j);
+            rk += (rj > rem) || (rj == rem && j < lane);
+          }
+          extra = (lane < nh && rk < left) ? 1 : 0;
+        }
+        qi = b + extra;
+        ures -= qi;
+      }
+      if (lane < nh) a.q[static_cast<int64_t>(r) * ncol + col] = qi + (t_i == r ? qloc_i : 0);
+    }
+  }
+  // CSR padding columns of Q
+  for (int j = E + nb + e; j < ncol; j += E)
+    for (int r = lane; r < R; r += kWave) a.q[static_cast<int64_t>(r) * ncol + j] = 0;
 }
 
 hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
-                       const ultraep_plan_buf &out, hipStream_t stream) {
+                       const ultraep_plan_buf &out, void *ws, hipStream_t stream) {
   PlanArgs a;
   a.load = load;
   a.R = g.R;
@@ -410,10 +691,15 @@ hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
   a.hs = out.host_pslot;
   a.q = out.reroute;
   a.stats = out.stats;
-  hipLaunchKernelGGL(k_plan_solve, dim3(1), dim3(kPlanThreads), 0, stream, a);
+  a.ws = carve(ws, g.R, g.E, g.n_slot);
+  hipLaunchKernelGGL(k_plan_prep, dim3(1), dim3(kPrepThreads), 0, stream, a);
   hipError_t err = hipGetLastError();
+  for (int round = 0; round < kRounds && err == hipSuccess; ++round) {
+    hipLaunchKernelGGL(k_plan_round, dim3(kNodes), dim3(kWave), 0, stream, a, round);
+    err = hipGetLastError();
+  }
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_plan_reroute, dim3(g.E), dim3(kWave), 0, stream, a);
+  hipLaunchKernelGGL(k_plan_finish, dim3(g.E), dim3(kWave), 0, stream, a);
   return hipGetLastError();
 }
 

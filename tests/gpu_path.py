@@ -45,6 +45,8 @@ def gpu_plan(load, g):
     plan = uep.Plan(g, DEV)
     for f in uep.PLAN_FIELDS:  # poison: every element must be written
         getattr(plan, f).fill_(-12345)
+    # the workspace's contents on entry must not matter
+    plan.ws.copy_(torch.randint(0, 256, plan.ws.shape, dtype=torch.uint8, device=DEV))
     uep.ultraep_plan(dev_i32(load), g, plan)
     torch.cuda.synchronize()
     return plan

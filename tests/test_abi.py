@@ -43,6 +43,13 @@ def test_plan_sizes():
             uep.ultraep_plan_sizes(bad)
 
 
+def test_plan_ws_bytes():
+    g = uep.Group(64, 256, 1, 1024)
+    n = uep.ultraep_plan_ws_bytes(g)
+    assert n >= 3 * 1023 * (1 + 2 * 64) * 4
+    assert uep.ultraep_plan_ws_bytes(uep.Group(3, 8, 1, 1)) == 0
+
+
 def test_ws_bytes():
     g = uep.Group(64, 256, 1, 1024)
     n = uep.ultraep_dispatch_ws_bytes(4096, 8, g)
@@ -63,10 +70,12 @@ def test_invalid_arguments_return_einval_without_launch():
     assert L.ultraep_count(fake, 8, 17, 16, 1, fake, fake, None) == E     # k > E
     assert L.ultraep_count(fake, 8, 2, 16, 0, fake, fake, None) == E      # no groups
     assert L.ultraep_count(fake, 8, 2, 16, 1, fake, None, None) == E      # no status
-    assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(pb), None) == E
+    assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(pb), fake, 1 << 30, None) == E
     bad = uep.Group(4, 15, 2, 32)
     full = uep.PlanBuf(*([4096] * 7))
-    assert L.ultraep_plan(fake, ctypes.byref(bad), ctypes.byref(full), None) == E
+    assert L.ultraep_plan(fake, ctypes.byref(bad), ctypes.byref(full), fake, 1 << 30, None) == E
+    assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(full), fake, 16, None) == E  # ws
+    assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(full), None, 1 << 30, None) == E
     assert L.ultraep_dispatch(fake, fake, 8, 2, 12, 0, ctypes.byref(g),  # H % 8
                               ctypes.byref(full), fake, fake, fake, fake, 1 << 20,
                               fake, None) == E
