@@ -2,10 +2,11 @@
 """Benchmark of the UltraEP per-layer balancing path on one MI355X.
 
 One step = one layer-microbatch of the hot path on the measured rank:
-  count  (that rank's top-k ids -> its row of the load matrix)
-  plan   (SolveReplication + SolveReroute over the whole EP group)
-  dispatch layout + row scatter (bf16 rows into per-replica send blocks)
-  pack   (replicated main-expert blobs into per-destination staging)
+  count      (that rank's top-k ids -> its row of the load matrix)
+  replicate  (SolveReplication over the whole EP group)
+  reroute    (SolveReroute)
+  dispatch   layout + row scatter (bf16 rows into per-replica send blocks)
+  pack       (replicated main-expert blobs into per-destination staging)
 on synthetic DeepSeek-V3-shaped training routing (E=256, top-8 with
 8-group / top-4-group restriction, EP=64, one redundant slot per rank,
 4096 tokens per rank, H=7168, F=2048).  The other 63 ranks' load rows are
@@ -13,9 +14,13 @@ resident inputs (the all-gather that delivers them is not on one GPU).  The
 measured rank is the one with the most outbound replica bytes.
 
 Timed region: K replays of the step captured in one HIP graph, bracketed by
-device synchronisation.  A second pass of K eager steps records HIP events
-around every launch on the launch stream; the dominant kernel's average
-duration gives the roofline figures.  The CPU oracle is timed
+device synchronisation.  Inside the graph the step follows the forward
+pipeline of Eq. (1): once SolveReplication is done, the weight packing runs
+on a second stream while reroute, layout and scatter run on the first; the
+two join at the end of the step.  The graph's outputs are checked against a
+sequential eager step.  A second pass of K sequential eager steps records
+HIP events around every launch on the launch stream; the dominant kernel's
+average duration gives the roofline figures.  The CPU oracle is timed
 single-threaded on a bounded sample of the same workload.
 
 Prints one JSON line.
@@ -118,7 +123,8 @@ def main():
 
     calls = [
         ("count", lambda: uep.ultraep_count(topk_r, T, k, c.E, 1, load_r, status)),
-        ("plan", lambda: uep.ultraep_plan(load, g, plan)),
+        ("plan_replicate", lambda: uep.ultraep_plan_replicate(load, g, plan)),
+        ("plan_reroute", lambda: uep.ultraep_plan_reroute(load, g, plan)),
         ("dispatch_layout", lambda: uep.ultraep_dispatch_layout(
             topk_r, T, k, rank, g, plan, ros, boff, ws, status)),
         ("dispatch_scatter", lambda: uep.ultraep_dispatch_scatter(
@@ -126,33 +132,54 @@ def main():
         ("pack", lambda: uep.ultraep_pack_replicas(
             w, W, rank, g, plan, staging, cap, doff, status)),
     ]
+    fn = dict(calls)
+    side = torch.cuda.Stream()  # default priority
 
     def step():
         for _, f in calls:
             f()
 
+    def step_overlapped():
+        fn["count"]()
+        fn["plan_replicate"]()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn["pack"]()  # needs only the replica placement
+        fn["plan_reroute"]()
+        fn["dispatch_layout"]()
+        fn["dispatch_scatter"]()
+        torch.cuda.current_stream().wait_stream(side)
+
+    outputs = (load_r, send, ros, boff, staging, doff,
+               *[getattr(plan, f) for f in uep.PLAN_FIELDS])
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    ref = [t.clone() for t in outputs]
 
     # ---------------- timed region: K graph replays of the whole step
     graph = torch.cuda.CUDAGraph()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
-        step()
+        step_overlapped()
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     with torch.cuda.graph(graph):
-        step()
+        step_overlapped()
+    for t in outputs:
+        t.fill_(-1)
     for _ in range(max(1, args.warmup)):
         graph.replay()
     torch.cuda.synchronize()
+    for a, b in zip(outputs, ref):
+        assert torch.equal(a, b), "graph replay differs from the eager step"
     t_start = time.perf_counter()
     for _ in range(args.steps):
         graph.replay()
     torch.cuda.synchronize()
     t_graph = (time.perf_counter() - t_start) / args.steps
+    del ref
 
     # ---------------- eager pass with HIP events around every launch
     stream = torch.cuda.current_stream()
@@ -228,7 +255,8 @@ def main():
             "routed_rows": n_routed,
             "replicas_shipped": int(n_out_r[rank]),
             "expert_blob_bytes": W_bytes,
-            "timed": "HIP graph replay of count+plan+dispatch+pack",
+            "timed": ("HIP graph replay of count, replicate, then "
+                      "{reroute, layout, scatter} alongside {pack}"),
         },
         "roofline": {
             "kernel": dom,
@@ -242,7 +270,8 @@ def main():
             "avg_launch_us": round(dus, 2),
         },
         "kernels_us": {n: round(v, 2) for n, v in per_call_us.items()},
-        "count_plan_us": round(per_call_us["count"] + per_call_us["plan"], 2),
+        "count_plan_us": round(per_call_us["count"] + per_call_us["plan_replicate"]
+                               + per_call_us["plan_reroute"], 2),
         "eager_us_per_step": round(t_eager * 1e6, 2),
         "dispatch_scatter_GBps": round(scatter_bytes / per_call_us["dispatch_scatter"] / 1e3, 1),
         "pack_GBps": round(pack_bytes / per_call_us["pack"] / 1e3, 1) if pack_bytes else None,

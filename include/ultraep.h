@@ -135,6 +135,19 @@ int ultraep_plan(const int32_t *load, const ultraep_group *g,
                  const ultraep_plan_buf *out, void *ws, size_t ws_bytes,
                  hipStream_t stream);
 
+/* The two halves of ultraep_plan, in this order on one stream (or with the
+ * second made to wait for the first): SolveReplication writes slot_expert,
+ * quota, host_ptr, host_rank, host_pslot and stats; SolveReroute then writes
+ * reroute from the load matrix and those buffers.  They are separate so a
+ * caller can run the reroute alongside the weight distribution
+ * (ultraep_pack_replicas needs only slot_expert), as in the forward pipeline
+ * of Sec. 4.2 and Eq. (1). */
+int ultraep_plan_replicate(const int32_t *load, const ultraep_group *g,
+                           const ultraep_plan_buf *out, void *ws, size_t ws_bytes,
+                           hipStream_t stream);
+int ultraep_plan_reroute(const int32_t *load, const ultraep_group *g,
+                         const ultraep_plan_buf *out, hipStream_t stream);
+
 /* Bytes of device workspace ultraep_plan needs for group *g (host only; 0
  * for an unsupported group): per-expert orders and the outcome and transfer
  * record of every speculatively evaluated bisection probe. */

@@ -78,6 +78,8 @@ def lib():
         L.ultraep_plan_sizes.argtypes = [gp, ctypes.POINTER(sz)]
         L.ultraep_count.argtypes = [_P, i64, i32, i32, i32, _P, _P, _P]
         L.ultraep_plan.argtypes = [_P, gp, pp, _P, sz, _P]
+        L.ultraep_plan_replicate.argtypes = [_P, gp, pp, _P, sz, _P]
+        L.ultraep_plan_reroute.argtypes = [_P, gp, pp, _P]
         L.ultraep_plan_ws_bytes.argtypes = [gp]
         L.ultraep_plan_ws_bytes.restype = sz
         L.ultraep_dispatch_ws_bytes.argtypes = [i64, i32, gp]
@@ -92,6 +94,7 @@ def lib():
         L.ultraep_strerror.argtypes = [ctypes.c_int]
         L.ultraep_strerror.restype = ctypes.c_char_p
         for f in ("ultraep_plan_sizes", "ultraep_count", "ultraep_plan",
+                  "ultraep_plan_replicate", "ultraep_plan_reroute",
                   "ultraep_dispatch", "ultraep_dispatch_layout",
                   "ultraep_dispatch_scatter", "ultraep_pack_replicas"):
             getattr(L, f).restype = ctypes.c_int
@@ -166,6 +169,19 @@ def ultraep_plan(load, g: Group, plan: Plan, ws=None, stream=None):
                                      ctypes.byref(plan.c), _ptr(ws),
                                      ws.numel() * ws.element_size(),
                                      _stream(stream)), "ultraep_plan")
+
+
+def ultraep_plan_replicate(load, g: Group, plan: Plan, ws=None, stream=None):
+    ws = plan.ws if ws is None else ws
+    return _check(lib().ultraep_plan_replicate(
+        _ptr(load), ctypes.byref(g), ctypes.byref(plan.c), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)), "ultraep_plan_replicate")
+
+
+def ultraep_plan_reroute(load, g: Group, plan: Plan, stream=None):
+    return _check(lib().ultraep_plan_reroute(
+        _ptr(load), ctypes.byref(g), ctypes.byref(plan.c), _stream(stream)),
+        "ultraep_plan_reroute")
 
 
 def ultraep_dispatch_ws_bytes(T, k, g: Group) -> int:

@@ -14,8 +14,10 @@ hipError_t launch_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
                         hipStream_t stream);
 
 size_t plan_ws_bytes(int32_t R, int32_t E, int32_t NS);
-hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
-                       const ultraep_plan_buf &out, void *ws, hipStream_t stream);
+hipError_t launch_plan_replicate(const int32_t *load, const ultraep_group &g,
+                                 const ultraep_plan_buf &out, void *ws, hipStream_t stream);
+hipError_t launch_plan_reroute(const int32_t *load, const ultraep_group &g,
+                               const ultraep_plan_buf &out, hipStream_t stream);
 
 // dispatch workspace carve-up
 struct DispatchWs {

@@ -18,12 +18,16 @@
 //                 largest slack (ties: lower rank) is one DPP wave max over a
 //                 packed (slack, rank) key; the accepted transfers are kept in
 //                 LDS and stored once at the end if the probe is feasible.
-//   k_plan_finish one wave per expert: walks all rounds to tau* and the last
-//                 feasible probe, materialises that probe's record into its
-//                 expert's row of U, its CSR host list, its rank's row of X, and
-//                 then splits the expert's load over its hosts (locality first,
-//                 then sources in ascending rank order by largest remainder
-//                 against the residual quotas).
+//   k_plan_emit   one wave per expert: walks the last round to tau* and the
+//                 last feasible probe, and materialises that probe's record
+//                 into its expert's row of U, its CSR host list and its rank's
+//                 row of X (SolveReplication ends here).
+//   k_plan_reroute one wave per expert: SolveReroute, locality first, then the
+//                 sources in ascending rank order split their residual demand
+//                 over the residual quotas by largest remainder.  It is a
+//                 separate entry point so that callers can run it alongside
+//                 the weight distribution, as the paper's forward pipeline
+//                 does (Eq. 1).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -248,7 +252,8 @@ __device__ __forceinline__ int wave_shl1(int v) {
 
 // One greedy feasibility probe at threshold tau, run by one wave.  Lane i
 // holds the i-th rank of the visiting order (rk_r) and its load (rk_l).
-// Returns the number of transfers if feasible, else a negative value.
+// Returns the number of transfers (recorded in s_re / s_rd) if feasible,
+// else a negative value.
 //
 // Admissible targets (slack > 0, a free slot) are kept as a list sorted by
 // (slack descending, rank ascending) across the lanes from the head `h`
@@ -256,14 +261,18 @@ __device__ __forceinline__ int wave_shl1(int v) {
 // its used-slot count beside it.  The list starts as the ranks in ascending
 // load order (the same order at every threshold) cut at load < tau.  A
 // transfer reads the head; a target whose slack or slots run out leaves the
-// list by advancing h, otherwise it moves back to its place in the order.
+// list by advancing h (always, with one slot per rank), otherwise it moves
+// back to its place in the order.  Transfer n is kept in lane n % 64 of two
+// registers, written to LDS every 64 transfers.
+template <bool kOneSlot>
 __device__ int probe_sorted(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
                             int as_r, int as_l, const int32_t *s_eorder,
                             const int32_t *s_elam, uint32_t *s_re, int32_t *s_rd) {
   int key = (lane < a.R && as_l < tau && a.NS > 0) ? ((tau - as_l) << 6) | (kWave - 1 - as_r) : 0;
   int used = 0;
-  int h = 0;
-  int n = 0;
+  int h = 0, n = 0;
+  uint32_t cur_et = 0;
+  int cur_d = 0;
   for (int oi = 0; oi < a.R; ++oi) {
     int exc = readlane(rk_l, oi) - tau;
     if (exc <= 0) break;  // the remaining ranks are not overloaded
@@ -289,30 +298,41 @@ __device__ int probe_sorted(const PlanArgs &a, int tau, int lane, int rk_r, int 
             if (min(exc, m) < a.u_min) return -1;
             break;  // bounded by this expert's remaining load: next expert
           }
-          const int ts = kWave - 1 - (kh & (kWave - 1));
-          const int uh = readlane(used, h) + 1;
-          if (m == d || uh >= a.NS) {
-            ++h;  // out of slack or slots
+          if (kOneSlot) {
+            ++h;
           } else {
-            const int nk = ((m - d) << 6) | (kh & (kWave - 1));
-            // new place p: after every listed key still larger than nk
-            const int p = h + __popcll(ballot(lane > h && key > nk));
-            const int ks = wave_shl1(key), us = wave_shl1(used);
-            const bool mv = lane >= h && lane < p;
-            key = mv ? ks : (lane == p ? nk : key);
-            used = mv ? us : (lane == p ? uh : used);
+            const int uh = readlane(used, h) + 1;
+            if (m == d || uh >= a.NS) {
+              ++h;  // out of slack or slots
+            } else {
+              const int nk = ((m - d) << 6) | (kh & (kWave - 1));
+              // new place p: after every listed key still larger than nk
+              const int p = h + __popcll(ballot(lane > h && key > nk));
+              const int ks = wave_shl1(key), us = wave_shl1(used);
+              const bool mv = lane >= h && lane < p;
+              key = mv ? ks : (lane == p ? nk : key);
+              used = mv ? us : (lane == p ? uh : used);
+            }
           }
-          if (lane == 0) {
-            s_re[n] = static_cast<uint32_t>(e) | (static_cast<uint32_t>(ts) << 16);
-            s_rd[n] = d;
-          }
+          const bool me = lane == (n & (kWave - 1));
+          cur_et = me ? (static_cast<uint32_t>(e) | (static_cast<uint32_t>(kWave - 1 - (kh & (kWave - 1))) << 16)) : cur_et;
+          cur_d = me ? d : cur_d;
           ++n;
+          if ((n & (kWave - 1)) == 0) {
+            s_re[n - kWave + lane] = cur_et;
+            s_rd[n - kWave + lane] = cur_d;
+          }
           exc -= d;
           cap -= d;
         }
       }
     }
     if (exc > 0) return -1;
+  }
+  const int base = n & ~(kWave - 1);
+  if (lane < (n & (kWave - 1))) {
+    s_re[base + lane] = cur_et;
+    s_rd[base + lane] = cur_d;
   }
   return n;
 }
@@ -460,8 +480,12 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
     const int rk_l = __shfl(ell_lane, rk_r);
     const int as_l = __shfl(ell_lane, as_r);
     __syncthreads();
-    n = packed ? probe_sorted(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd)
-               : probe_wide(a, tau, lane, rk_r, rk_l, ell_lane, s_eorder, s_elam, s_re, s_rd);
+    if (!packed)
+      n = probe_wide(a, tau, lane, rk_r, rk_l, ell_lane, s_eorder, s_elam, s_re, s_rd);
+    else if (a.NS == 1)
+      n = probe_sorted<true>(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
+    else
+      n = probe_sorted<false>(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
     if (n > 0) {
       __syncthreads();
       uint32_t *rec = a.ws.rec + (static_cast<int64_t>(round) * kNodes + b) * 2 * RS;
@@ -474,9 +498,9 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
   if (lane == 0) a.ws.res[round * kNodes + b] = n;
 }
 
-// ---------------------------------------------------------------- finish
+// ---------------------------------------------------------------- emit
 
-__global__ void __launch_bounds__(kWave) k_plan_finish(PlanArgs a) {
+__global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   __shared__ int32_t s_res[kNodes];
   __shared__ uint32_t s_et[kMaxRec];
   __shared__ int32_t s_d[kMaxRec];
@@ -559,6 +583,7 @@ __global__ void __launch_bounds__(kWave) k_plan_finish(PlanArgs a) {
   for (int i = 0; i < nh; ++i)
     if (s_ht[i] == lane) u_r = s_hu[i];
   if (lane < R) a.U[static_cast<int64_t>(e) * R + lane] = u_r;
+  (void)ncol;
   // row t = e of X (one workgroup per rank): slots in acceptance order
   if (e < R && NS > 0) {
     int cnt = 0;
@@ -590,91 +615,102 @@ __global__ void __launch_bounds__(kWave) k_plan_finish(PlanArgs a) {
       a.stats[7] = a.ws.hdr[2];
     }
   }
+}
 
-  // ---- SolveReroute for expert e ------------------------------------------
+// ---------------------------------------------------------------- reroute
+
+// SolveReroute for expert blockIdx.x: hosts and quotas from the CSR lists
+// and U written by k_plan_emit, the expert's column of the load matrix.
+template <bool kExact, bool kOneRow>
+__device__ void split_expert(const PlanArgs &a, int e, int lane, int j0, int nh, int lam_r,
+                             int u_r, int t_i, int u_i) {
+  const int R = a.R, ncol = a.ncol;
+  // locality: a source that hosts e first consumes its own quota
+  const int loc_r = min(lam_r, u_r);
+  const int lamhat_r = lam_r - loc_r;
+  const int qloc_i = __shfl(loc_r, t_i);
+  int ures = lane < nh ? u_i - qloc_i : 0;
+  // residual quota total seen by source r: D_0 minus the demand of the
+  // sources before it; its reciprocal, all computed lane-parallel up front
+  int incl = lamhat_r;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  const int D0 = wave_sum(ures);
+  const int Dr = D0 - (incl - lamhat_r);
+  const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
+  int32_t *qcol = a.q + j0 + lane;
+  for (int r = 0; r < R; ++r) {
+    const int lh = readlane(lamhat_r, r);
+    int qi = 0;
+    if (lh > 0) {
+      const int D = readlane(Dr, r);
+      const double rD = readlane_d(rDr, r);
+      // floor(lh * ures / D): fp64 estimate (far below one unit off since
+      // the quotient is < 2^30), made exact by one correction
+      int b, rem;
+      if (kExact) {  // all operands below 2^26: products below 2^52, exact
+        const double Dd = static_cast<double>(D);
+        const double pr = static_cast<double>(lh) * static_cast<double>(ures);
+        double bq = __builtin_trunc(pr * rD);
+        double rd = __builtin_fma(-bq, Dd, pr);
+        const bool lo = rd < 0.0, hi = rd >= Dd;
+        bq += lo ? -1.0 : (hi ? 1.0 : 0.0);
+        rd += lo ? Dd : (hi ? -Dd : 0.0);
+        b = static_cast<int>(bq);
+        rem = static_cast<int>(rd);
+      } else {
+        b = static_cast<int>(static_cast<double>(lh) * static_cast<double>(ures) * rD);
+        int64_t rm = static_cast<int64_t>(lh) * ures - static_cast<int64_t>(b) * D;
+        const bool lo = rm < 0, hi = rm >= D;
+        b += lo ? -1 : (hi ? 1 : 0);
+        rm += lo ? D : (hi ? -D : 0);
+        rem = static_cast<int>(rm);
+      }
+      const int left = lh - (kOneRow ? readlane(row_sum(b), 0) : wave_sum(b));
+      int extra = 0;
+      if (left > 0) {  // the `left` hosts with the largest remainders
+        int rk = 0;
+        for (int j = 0; j < nh; ++j) {
+          const int rj = readlane(rem, j);
+          rk += (rj > rem) || (rj == rem && j < lane);
+        }
+        extra = (lane < nh && rk < left) ? 1 : 0;
+      }
+      qi = b + extra;
+      ures -= qi;
+    }
+    if (lane < nh) qcol[static_cast<int64_t>(r) * ncol] = qi + (t_i == r ? qloc_i : 0);
+  }
+}
+
+__global__ void __launch_bounds__(kWave) k_plan_reroute(PlanArgs a) {
+  const int e = blockIdx.x, lane = threadIdx.x;
+  const int R = a.R, E = a.E, ncol = a.ncol;
+  if (a.stats[6] != 0) return;
+  const int j0 = a.hp[e], nh = a.hp[e + 1] - j0, total = a.hp[E];
   const int lam_r = lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
   if (nh == 1) {
-    if (lane < R) a.q[static_cast<int64_t>(lane) * ncol + hp_e] = lam_r;
+    if (lane < R) a.q[static_cast<int64_t>(lane) * ncol + j0] = lam_r;
   } else {
-    // locality: a source that hosts e first consumes its own quota
-    const int loc_r = min(lam_r, u_r);
-    const int lamhat_r = lam_r - loc_r;
-    const int t_i = lane < nh ? s_ht[lane] : 0;
-    const int qloc_i = __shfl(loc_r, t_i);
-    int ures = lane < nh ? s_hu[lane] - qloc_i : 0;
-    // residual quota total seen by source r: D_0 minus the demand of the
-    // sources before it; its reciprocal, all computed lane-parallel up front
-    int incl = lamhat_r;
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int t = __shfl_up(incl, o);
-      if (lane >= o) incl += t;
-    }
-    const int D0 = wave_sum(ures);
-    const int Dr = D0 - (incl - lamhat_r);
-    const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
-    const bool one_row = nh <= 16;
-    // loads below 2^26: every product below 2^52, so fp64 is exact
-    const bool exact_fp64 = a.ws.hdr[2] < (int64_t(1) << 26);
-    const int64_t col = hp_e + lane;
-    for (int r = 0; r < R; ++r) {
-      const int lh = readlane(lamhat_r, r);
-      int qi = 0;
-      if (lh > 0) {
-        const int D = readlane(Dr, r);
-        const double rD = readlane_d(rDr, r);
-        // floor(lh * ures / D): fp64 estimate (far below one unit off since
-        // the quotient is < 2^30), made exact by one correction
-        int b, rem;
-        if (exact_fp64) {
-          const double Dd = static_cast<double>(D);
-          const double pr = static_cast<double>(lh) * static_cast<double>(ures);
-          double bq = __builtin_trunc(pr * rD);
-          double rd = __builtin_fma(-bq, Dd, pr);
-          if (rd < 0.0) {
-            bq -= 1.0;
-            rd += Dd;
-          } else if (rd >= Dd) {
-            bq += 1.0;
-            rd -= Dd;
-          }
-          b = static_cast<int>(bq);
-          rem = static_cast<int>(rd);
-        } else {
-          b = static_cast<int>(static_cast<double>(lh) * static_cast<double>(ures) * rD);
-          int64_t rm = static_cast<int64_t>(lh) * ures - static_cast<int64_t>(b) * D;
-          if (rm < 0) {
-            --b;
-            rm += D;
-          } else if (rm >= D) {
-            ++b;
-            rm -= D;
-          }
-          rem = static_cast<int>(rm);
-        }
-        const int left = lh - (one_row ? readlane(row_sum(b), 0) : wave_sum(b));
-        int extra = 0;
-        if (left > 0) {  // the `left` hosts with the largest remainders
-          int rk = 0;
-          for (int j = 0; j < nh; ++j) {
-            const int rj = readlane(rem, j);
-            rk += (rj > rem) || (rj == rem && j < lane);
-          }
-          extra = (lane < nh && rk < left) ? 1 : 0;
-        }
-        qi = b + extra;
-        ures -= qi;
-      }
-      if (lane < nh) a.q[static_cast<int64_t>(r) * ncol + col] = qi + (t_i == r ? qloc_i : 0);
-    }
+    const int u_r = lane < R ? a.U[static_cast<int64_t>(e) * R + lane] : 0;
+    const int t_i = lane < nh ? a.hr[j0 + lane] : 0;
+    const int u_i = __shfl(u_r, t_i);
+    const bool exact = a.stats[7] < (int64_t(1) << 26);
+    if (exact && nh <= 16) split_expert<true, true>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
+    else if (exact) split_expert<true, false>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
+    else if (nh <= 16) split_expert<false, true>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
+    else split_expert<false, false>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
   }
   // CSR padding columns of Q
-  for (int j = E + nb + e; j < ncol; j += E)
+  for (int j = total + e; j < ncol; j += E)
     for (int r = lane; r < R; r += kWave) a.q[static_cast<int64_t>(r) * ncol + j] = 0;
 }
 
-hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
-                       const ultraep_plan_buf &out, void *ws, hipStream_t stream) {
-  PlanArgs a;
+static PlanArgs plan_args(const int32_t *load, const ultraep_group &g,
+                          const ultraep_plan_buf &out, void *ws) {
+  PlanArgs a{};
   a.load = load;
   a.R = g.R;
   a.E = g.E;
@@ -691,7 +727,13 @@ hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
   a.hs = out.host_pslot;
   a.q = out.reroute;
   a.stats = out.stats;
-  a.ws = carve(ws, g.R, g.E, g.n_slot);
+  if (ws) a.ws = carve(ws, g.R, g.E, g.n_slot);
+  return a;
+}
+
+hipError_t launch_plan_replicate(const int32_t *load, const ultraep_group &g,
+                                 const ultraep_plan_buf &out, void *ws, hipStream_t stream) {
+  const PlanArgs a = plan_args(load, g, out, ws);
   hipLaunchKernelGGL(k_plan_prep, dim3(1), dim3(kPrepThreads), 0, stream, a);
   hipError_t err = hipGetLastError();
   for (int round = 0; round < kRounds && err == hipSuccess; ++round) {
@@ -699,7 +741,14 @@ hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
     err = hipGetLastError();
   }
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_plan_finish, dim3(g.E), dim3(kWave), 0, stream, a);
+  hipLaunchKernelGGL(k_plan_emit, dim3(g.E), dim3(kWave), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan_reroute(const int32_t *load, const ultraep_group &g,
+                               const ultraep_plan_buf &out, hipStream_t stream) {
+  const PlanArgs a = plan_args(load, g, out, nullptr);
+  hipLaunchKernelGGL(k_plan_reroute, dim3(g.E), dim3(kWave), 0, stream, a);
   return hipGetLastError();
 }
 

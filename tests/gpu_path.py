@@ -41,13 +41,20 @@ def gpu_count(topk_all, E):
     return counts.cpu().numpy(), int(st.item())
 
 
-def gpu_plan(load, g):
+def gpu_plan(load, g, split=False):
+    """split: SolveReplication and SolveReroute through their own entry points
+    instead of ultraep_plan."""
     plan = uep.Plan(g, DEV)
     for f in uep.PLAN_FIELDS:  # poison: every element must be written
         getattr(plan, f).fill_(-12345)
     # the workspace's contents on entry must not matter
     plan.ws.copy_(torch.randint(0, 256, plan.ws.shape, dtype=torch.uint8, device=DEV))
-    uep.ultraep_plan(dev_i32(load), g, plan)
+    ld = dev_i32(load)
+    if split:
+        uep.ultraep_plan_replicate(ld, g, plan)
+        uep.ultraep_plan_reroute(ld, g, plan)
+    else:
+        uep.ultraep_plan(ld, g, plan)
     torch.cuda.synchronize()
     return plan
 

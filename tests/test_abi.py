@@ -21,6 +21,8 @@ def declared_symbols():
 def test_header_declares_the_entry_points():
     names = declared_symbols()
     for n in ("ultraep_count", "ultraep_plan", "ultraep_dispatch",
+              "ultraep_plan_replicate", "ultraep_plan_reroute",
+              "ultraep_dispatch_layout", "ultraep_dispatch_scatter",
               "ultraep_pack_replicas", "ultraep_plan_sizes",
               "ultraep_dispatch_ws_bytes", "ultraep_strerror"):
         assert n in names
@@ -76,6 +78,12 @@ def test_invalid_arguments_return_einval_without_launch():
     assert L.ultraep_plan(fake, ctypes.byref(bad), ctypes.byref(full), fake, 1 << 30, None) == E
     assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(full), fake, 16, None) == E  # ws
     assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(full), None, 1 << 30, None) == E
+    assert L.ultraep_plan_replicate(fake, ctypes.byref(g), ctypes.byref(full), fake, 16,
+                                    None) == E
+    assert L.ultraep_plan_replicate(None, ctypes.byref(g), ctypes.byref(full), fake,
+                                    1 << 30, None) == E
+    assert L.ultraep_plan_reroute(fake, ctypes.byref(bad), ctypes.byref(full), None) == E
+    assert L.ultraep_plan_reroute(fake, ctypes.byref(g), ctypes.byref(pb), None) == E
     assert L.ultraep_dispatch(fake, fake, 8, 2, 12, 0, ctypes.byref(g),  # H % 8
                               ctypes.byref(full), fake, fake, fake, fake, 1 << 20,
                               fake, None) == E

@@ -46,6 +46,15 @@ def test_count_and_plan_workloads(cid, m):
     check_plan(ocounts, og, op)
 
 
+@pytest.mark.parametrize("cid,m", [(1, 1), (2, 3), (4, 2), (5, 9)])
+def test_split_plan_entry_points(cid, m):
+    """SolveReplication then SolveReroute through their own entry points give
+    the same plan as ultraep_plan."""
+    c, g, og, tk = _workload(cid, m)
+    load, _ = oracle.count(tk, c.E, c.R)
+    gp.assert_plan_equal(gp.gpu_plan(load, g, split=True), oracle.plan(load, og))
+
+
 def test_qwen3_all_microbatches():
     c = gen.config(3)
     g, og = gp.groups(c.R, c.E, c.n_slot, c.u_min)
@@ -185,10 +194,12 @@ def test_repeated_runs_identical():
         assert all(np.array_equal(u, v) for u, v in zip(a[:3], b[:3]))
 
 
-def test_graph_replay_matches_eager():
+@pytest.mark.parametrize("fork", [False, True])
+def test_graph_replay_matches_eager(fork):
     """count -> plan -> dispatch -> pack captured in one HIP graph, replayed
     several times with eager work in between; every replay must equal the
-    eager result."""
+    eager result.  fork: the pipeline the benchmark times, with the pack on a
+    second stream after SolveReplication, alongside reroute and dispatch."""
     c, g, og, tk_all = _workload(1, 2)
     r = 2
     T, k, H = c.T, c.k, c.H
@@ -209,11 +220,23 @@ def test_graph_replay_matches_eager():
     stg = torch.zeros((cap, W), dtype=torch.int16, device=gp.DEV)
     doff = torch.empty(c.R + 1, dtype=torch.int64, device=gp.DEV)
 
+    side = torch.cuda.Stream()
+
     def step():
         uep.ultraep_count(tk_all_d, T, k, c.E, c.R, load, st)
-        uep.ultraep_plan(load, g, plan)
-        uep.ultraep_dispatch(x, tk_r, T, k, H, r, g, plan, send, ros, boff, ws, st)
-        uep.ultraep_pack_replicas(w, W, r, g, plan, stg, cap, doff, st)
+        if not fork:
+            uep.ultraep_plan(load, g, plan)
+            uep.ultraep_dispatch(x, tk_r, T, k, H, r, g, plan, send, ros, boff, ws, st)
+            uep.ultraep_pack_replicas(w, W, r, g, plan, stg, cap, doff, st)
+            return
+        uep.ultraep_plan_replicate(load, g, plan)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            uep.ultraep_pack_replicas(w, W, r, g, plan, stg, cap, doff, st)
+        uep.ultraep_plan_reroute(load, g, plan)
+        uep.ultraep_dispatch_layout(tk_r, T, k, r, g, plan, ros, boff, ws, st)
+        uep.ultraep_dispatch_scatter(x, T, k, H, ros, boff[-1:], send)
+        torch.cuda.current_stream().wait_stream(side)
 
     outs = lambda: [t.clone() for t in (load, send, ros, boff, stg, doff,
                                         *[getattr(plan, f) for f in uep.PLAN_FIELDS])]
