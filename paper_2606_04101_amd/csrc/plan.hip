@@ -43,10 +43,12 @@ constexpr int64_t kMaxLoad = int64_t(1) << 30;
 constexpr int kNotReached = INT32_MIN;
 constexpr int kPrepThreads = 1024;
 constexpr int kHdr = 4 + 4 * kRounds;  // int64 header words
+constexpr int kBitWords = (kNodes + 63) / 64;  // outcome bits per round
 
 struct PlanWs {
   int64_t *hdr;        // [4] tau_lo0, tau_hi0, L, status, then per round j the
                        // bisection state after rounds 0..j: lo, hi, best, probes
+  uint64_t *bits;      // [kRounds][kBitWords] feasible probes, one bit per node
   int32_t *ell;        // [R]
   int32_t *rank_desc;  // [R] ranks by descending load (visiting order)
   int32_t *rank_asc;   // [R] ranks by ascending load (target order)
@@ -60,14 +62,15 @@ struct PlanWs {
 size_t plan_ws_bytes(int32_t R, int32_t E, int32_t NS) {
   const int64_t RS = static_cast<int64_t>(R) * NS;
   const int64_t ints = 3 * R + 3 * E + int64_t(kRounds) * kNodes * (1 + 2 * RS);
-  return static_cast<size_t>(kHdr * 8 + (ints * 4 + 255) / 256 * 256);
+  return static_cast<size_t>(kHdr * 8 + kRounds * kBitWords * 8 + (ints * 4 + 255) / 256 * 256);
 }
 
 static PlanWs carve(void *ws, int32_t R, int32_t E, int32_t NS) {
   (void)NS;
   PlanWs w;
   w.hdr = static_cast<int64_t *>(ws);
-  int32_t *p = reinterpret_cast<int32_t *>(w.hdr + kHdr);
+  w.bits = reinterpret_cast<uint64_t *>(w.hdr + kHdr);
+  int32_t *p = reinterpret_cast<int32_t *>(w.bits + kRounds * kBitWords);
   w.ell = p;
   p += R;
   w.rank_desc = p;
@@ -97,6 +100,11 @@ struct PlanArgs {
 };
 
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint64_t uni64(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
 
 __device__ __forceinline__ double readlane_d(double v, int l) {
   const long long b = __double_as_longlong(v);
@@ -118,6 +126,7 @@ __global__ void __launch_bounds__(kPrepThreads) k_plan_prep(PlanArgs a) {
     s_L = 0;
     s_bad = 0;
   }
+  if (tid < kRounds * kBitWords) a.ws.bits[tid] = 0;
   __syncthreads();
   // lambda_e: thread (part, e) sums rows part, part + parts, ... with up to
   // 16 loads in flight, the parts are then combined in LDS
@@ -180,23 +189,30 @@ __global__ void __launch_bounds__(kPrepThreads) k_plan_prep(PlanArgs a) {
     a.ws.elam[r * nm + pos] = l;
   }
   __syncthreads();
-  if (tid < kWave) {  // ranks by descending load (ties: lower rank); R <= 64
-    const int l = tid < R ? s_ell[tid] : -1;
-    if (tid < R) {
-      int pos = 0;
-      for (int r = 0; r < R; ++r) {
-        const int lr = s_ell[r];
-        pos += (lr > l) || (lr == l && r < tid);
+  {  // ranks by descending and by ascending load (ties: lower rank): 16
+     // threads per rank each compare it with 4 others, then a DPP row sum
+    const int i = tid >> 4, part = tid & 15;
+    int cnt = 0;  // ranks ahead in descending order << 16 | ahead in ascending
+    if (i < R) {
+      const int li = s_ell[i];
+#pragma unroll
+      for (int k = 0; k < kMaxR / 16; ++k) {
+        const int r = part * (kMaxR / 16) + k;
+        if (r < R) {
+          const int lr = s_ell[r];
+          const bool tie = lr == li && r < i;
+          cnt += ((lr > li || tie) ? (1 << 16) : 0) + ((lr < li || tie) ? 1 : 0);
+        }
       }
-      a.ws.rank_desc[pos] = tid;
-      int apos = 0;  // ascending load, ties: lower rank
-      for (int r = 0; r < R; ++r) {
-        const int lr = s_ell[r];
-        apos += (lr < l) || (lr == l && r < tid);
-      }
-      a.ws.rank_asc[apos] = tid;
     }
-    const int hi = wave_max(l);
+    cnt = row_sum(cnt);
+    if (i < R && part == 0) {
+      a.ws.rank_desc[cnt >> 16] = i;
+      a.ws.rank_asc[cnt & 0xFFFF] = i;
+    }
+  }
+  if (tid < kWave) {
+    const int hi = wave_max(tid < R ? s_ell[tid] : -1);
     if (tid == 0) {
       const int64_t m = (L + R - 1) / R;
       const int64_t lo = (a.beta_num * m + a.beta_den - 1) / a.beta_den;
@@ -210,131 +226,198 @@ __global__ void __launch_bounds__(kPrepThreads) k_plan_prep(PlanArgs a) {
 
 // ---------------------------------------------------------------- rounds
 
-// Walks the depth-kDepth subtree of one round over its stored outcomes
-// (s_res), from [lo, hi): updates the interval, the last feasible node and
-// the number of probes of the sequential bisection.
-__device__ void walk_round(const int32_t *s_res, int64_t &lo, int64_t &hi, int &best,
-                           int &n_probe) {
-  int node = 0;
-  for (int d = 0; d < kDepth && lo < hi; ++d) {
-    const int64_t mid = (lo + hi) / 2;
-    ++n_probe;
-    if (uni(s_res[node]) >= 0) {
-      hi = mid;
-      best = node;
-      node = 2 * node + 1;
-    } else {
-      lo = mid + 1;
-      node = 2 * node + 2;
-    }
-  }
-}
-
-// All kNodes outcomes of one round into LDS: 16 independent loads per lane.
-__device__ void load_round(const int32_t *res, int32_t *s_res, int lane) {
-  int v[16];
-#pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int i = u * kWave + lane;
-    v[u] = i < kNodes ? __builtin_nontemporal_load(res + i) : 0;
-  }
-#pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int i = u * kWave + lane;
-    if (i < kNodes) s_res[i] = v[u];
-  }
-}
-
 // DPP wave_shl:1 - lane i receives lane i+1 (lane 63 keeps its value)
 __device__ __forceinline__ int wave_shl1(int v) {
   return __builtin_amdgcn_update_dpp(v, v, 0x130, 0xF, 0xF, false);
 }
 
-// One greedy feasibility probe at threshold tau, run by one wave.  Lane i
-// holds the i-th rank of the visiting order (rk_r) and its load (rk_l).
-// Returns the number of transfers (recorded in s_re / s_rd) if feasible,
-// else a negative value.
+// Greedy feasibility probes of SolveReplication at threshold tau (Sec. 5.1),
+// one wave each.  Lane i holds the i-th rank of the visiting order (rk_r,
+// rank, and rk_l, its load: descending load, ties to the lower rank) and
+// the i-th rank of ascending load (as_r, as_l).  A probe returns the number
+// of accepted transfers, recorded in s_re / s_rd as (e | t << 16, delta) in
+// acceptance order, or -1 if the threshold is infeasible.
 //
-// Admissible targets (slack > 0, a free slot) are kept as a list sorted by
-// (slack descending, rank ascending) across the lanes from the head `h`
-// on, each as a packed key (slack << 6) | (63 - rank) (slacks < 2^25) with
-// its used-slot count beside it.  The list starts as the ranks in ascending
-// load order (the same order at every threshold) cut at load < tau.  A
-// transfer reads the head; a target whose slack or slots run out leaves the
-// list by advancing h (always, with one slot per rank), otherwise it moves
-// back to its place in the order.  Transfer n is kept in lane n % 64 of two
-// registers, written to LDS every 64 transfers.
-template <bool kOneSlot>
-__device__ int probe_sorted(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
-                            int as_r, int as_l, const int32_t *s_eorder,
-                            const int32_t *s_elam, uint32_t *s_re, int32_t *s_rd) {
-  int key = (lane < a.R && as_l < tau && a.NS > 0) ? ((tau - as_l) << 6) | (kWave - 1 - as_r) : 0;
+// The admissible targets (slack > 0, a free slot) form a list sorted by
+// slack descending, rank ascending, one per lane from the head h on.  It
+// starts as the ranks of load below tau in ascending load order.  With the
+// slacks m in lanes and their inclusive prefix P (B = P before the head),
+// an expert that has to shed need = min(excess, its load) takes whole every
+// target from the head whose running slack stays below need (one ballot),
+// then the rest d from the next target.  A whole transfer is bound by the
+// target's slack, so one below u_min makes the probe infeasible, and the
+// target leaves the list, exactly as transfer-by-transfer evaluation finds.
+// The experts are visited in one flat loop (rank by rank, experts by
+// descending load) with scalar loop state and a single exit.
+
+// Loads experts [j0, j0 + 64) of rank r's visiting order into lanes.
+__device__ __forceinline__ void load_experts(const PlanArgs &a, int r, int j0, int lane,
+                                             const int32_t *s_eorder, const int32_t *s_elam,
+                                             int &ev, int &lv) {
+  const int jl = j0 + lane;
+  ev = jl < a.nm ? s_eorder[r * a.nm + jl] : 0;
+  lv = jl < a.nm ? s_elam[r * a.nm + jl] : 0;
+}
+
+// One redundant slot per rank: every transfer uses up its target, so
+// transfer k goes to the k-th listed target and its record stays in lane k.
+__device__ int probe_one_slot(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
+                              int as_r, int as_l, const int32_t *s_eorder,
+                              const int32_t *s_elam, uint32_t *s_re, int32_t *s_rd) {
+  const int R = a.R, nm = a.nm, u_min = a.u_min;
+  const bool tv = lane < R && as_l < tau;
+  const int m = tv ? tau - as_l : 0;
+  const uint64_t tmask = ballot(tv);  // a prefix of the lanes
+  const int nT = __popcll(tmask);
+  // inclusive prefix of the slacks: each is below 2^25, the sum below 2^31
+  int P = m;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(P, o);
+    if (lane >= o) P += t;
+  }
+  const uint64_t low_umin = ballot(tv && m < u_min);
+  int x = readlane(rk_l, 0) - tau;
+  if (x <= 0) return 0;  // nothing to shed
+  int r = readlane(rk_r, 0);
+  int ev, lv;
+  load_experts(a, r, 0, lane, s_eorder, s_elam, ev, lv);
+  int rec_e = 0, rec_d = 0;
+  int h = 0, B = 0, oi = 0, j = 0;  // head, slack before it, rank, expert
+  bool fail = false;
+  for (;;) {
+    const int c = readlane(lv, j & (kWave - 1));
+    const int e = readlane(ev, j & (kWave - 1));
+    // an expert with no load left: the rank's excess cannot be shed
+    fail = c <= 0 || h >= nT;
+    if (fail) break;
+    const int need = min(x, c);
+    const uint64_t whole = uni64(ballot(P - B < need) & tmask & (~uint64_t(0) << h));
+    const int hh = uni(h + __popcll(whole));
+    fail = (whole & low_umin) != 0 || hh >= nT;
+    if (fail) break;
+    const bool wl = (whole >> lane) & 1;
+    rec_e = wl ? e : rec_e;
+    rec_d = wl ? m : rec_d;
+    const int Ph = readlane(P, hh), mh = readlane(m, hh);
+    const int taken = Ph - mh - B;  // slack of the whole targets
+    const int d = need - taken;     // the rest, at most mh
+    x -= taken;
+    const bool take = d >= u_min;
+    // d below u_min: infeasible unless only this expert's load is short
+    fail = !take && min(x, mh) < u_min;
+    if (fail) break;
+    rec_e = (take && lane == hh) ? e : rec_e;
+    rec_d = (take && lane == hh) ? d : rec_d;
+    x -= take ? d : 0;
+    B = uni(take ? Ph : Ph - mh);
+    h = uni(take ? hh + 1 : hh);
+    if (x > 0 && ++j < nm) {  // next expert of this rank
+      if ((j & (kWave - 1)) == 0) load_experts(a, r, j, lane, s_eorder, s_elam, ev, lv);
+      continue;
+    }
+    fail = x > 0;  // the rank's experts ran out
+    if (fail || ++oi >= R) break;
+    x = readlane(rk_l, oi) - tau;
+    if (x <= 0) break;  // the remaining ranks are not overloaded
+    r = readlane(rk_r, oi);
+    load_experts(a, r, 0, lane, s_eorder, s_elam, ev, lv);
+    j = 0;
+  }
+  if (fail) return -1;
+  if (lane < h) {
+    s_re[lane] = static_cast<uint32_t>(rec_e) | (static_cast<uint32_t>(as_r) << 16);
+    s_rd[lane] = rec_d;
+  }
+  return h;
+}
+
+// Several redundant slots per rank: a target that keeps slack and a free
+// slot after an expert's last (partial) transfer moves back to its place in
+// the list; the lanes it passes shift down by one (DPP) and P is patched.
+// The list entries are packed keys (slack << 6) | (63 - rank).
+__device__ int probe_multi(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
+                           int as_r, int as_l, const int32_t *s_eorder,
+                           const int32_t *s_elam, uint32_t *s_re, int32_t *s_rd) {
+  const int R = a.R, nm = a.nm, NS = a.NS, u_min = a.u_min;
+  const bool tv = lane < R && as_l < tau && NS > 0;
+  int key = tv ? ((tau - as_l) << 6) | (kWave - 1 - as_r) : 0;
   int used = 0;
-  int h = 0, n = 0;
-  uint32_t cur_et = 0;
-  int cur_d = 0;
-  for (int oi = 0; oi < a.R; ++oi) {
-    int exc = readlane(rk_l, oi) - tau;
-    if (exc <= 0) break;  // the remaining ranks are not overloaded
-    const int r = readlane(rk_r, oi);
-    for (int j0 = 0; j0 < a.nm && exc > 0; j0 += kWave) {
-      const int jl = j0 + lane;
-      const int ev = jl < a.nm ? s_eorder[r * a.nm + jl] : 0;
-      const int lv = jl < a.nm ? s_elam[r * a.nm + jl] : 0;
-      const int jn = min(kWave, a.nm - j0);
-      for (int j = 0; j < jn && exc > 0; ++j) {
-        const int e = readlane(ev, j);
-        int cap = readlane(lv, j);
-        while (exc > 0 && cap > 0) {
-          // no admissible rank: the same holds for every later expert of r
-          if (h >= kWave) return -1;
-          const int kh = readlane(key, h);
-          if (kh == 0) return -1;
-          const int m = kh >> 6;
-          const int d = min(min(exc, m), cap);
-          if (d < a.u_min) {
-            // bounded by the excess or the slack: every later expert of r
-            // meets the same bound, so r keeps its excess
-            if (min(exc, m) < a.u_min) return -1;
-            break;  // bounded by this expert's remaining load: next expert
-          }
-          if (kOneSlot) {
-            ++h;
-          } else {
-            const int uh = readlane(used, h) + 1;
-            if (m == d || uh >= a.NS) {
-              ++h;  // out of slack or slots
-            } else {
-              const int nk = ((m - d) << 6) | (kh & (kWave - 1));
-              // new place p: after every listed key still larger than nk
-              const int p = h + __popcll(ballot(lane > h && key > nk));
-              const int ks = wave_shl1(key), us = wave_shl1(used);
-              const bool mv = lane >= h && lane < p;
-              key = mv ? ks : (lane == p ? nk : key);
-              used = mv ? us : (lane == p ? uh : used);
-            }
-          }
-          const bool me = lane == (n & (kWave - 1));
-          cur_et = me ? (static_cast<uint32_t>(e) | (static_cast<uint32_t>(kWave - 1 - (kh & (kWave - 1))) << 16)) : cur_et;
-          cur_d = me ? d : cur_d;
-          ++n;
-          if ((n & (kWave - 1)) == 0) {
-            s_re[n - kWave + lane] = cur_et;
-            s_rd[n - kWave + lane] = cur_d;
-          }
-          exc -= d;
-          cap -= d;
-        }
+  const uint64_t live = ballot(tv);  // a prefix of the lanes; its length never changes
+  const int nT = __popcll(live);
+  int P = key >> 6;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(P, o);
+    if (lane >= o) P += t;
+  }
+  int x = readlane(rk_l, 0) - tau;
+  if (x <= 0) return 0;
+  int r = readlane(rk_r, 0);
+  int ev, lv;
+  load_experts(a, r, 0, lane, s_eorder, s_elam, ev, lv);
+  int h = 0, B = 0, n = 0, oi = 0, j = 0;
+  bool fail = false;
+  for (;;) {
+    const int c = readlane(lv, j & (kWave - 1));
+    const int e = readlane(ev, j & (kWave - 1));
+    fail = c <= 0 || h >= nT;
+    if (fail) break;
+    const int need = min(x, c);
+    const int m = key >> 6;
+    const uint64_t whole = uni64(ballot(P - B < need) & live & (~uint64_t(0) << h));
+    const uint64_t low = uni64(ballot(m < u_min));
+    const int hh = uni(h + __popcll(whole));
+    fail = (whole & low) != 0 || hh >= nT;
+    if (fail) break;
+    if ((whole >> lane) & 1) {
+      s_re[n + lane - h] = static_cast<uint32_t>(e) |
+                           (static_cast<uint32_t>(kWave - 1 - (key & (kWave - 1))) << 16);
+      s_rd[n + lane - h] = m;
+    }
+    n += hh - h;
+    const int Ph = readlane(P, hh), kh = readlane(key, hh);
+    const int mh = kh >> 6;
+    const int taken = Ph - mh - B;
+    const int d = need - taken;
+    x -= taken;
+    const bool take = d >= u_min;
+    fail = !take && min(x, mh) < u_min;
+    if (fail) break;
+    B = Ph - mh;
+    h = hh;
+    if (take) {
+      if (lane == 0) {
+        s_re[n] = static_cast<uint32_t>(e) | (static_cast<uint32_t>(kWave - 1 - (kh & (kWave - 1))) << 16);
+        s_rd[n] = d;
+      }
+      ++n;
+      x -= d;
+      const int uh = readlane(used, hh) + 1;
+      if (mh == d || uh >= NS) {  // out of slack or slots: leaves the list
+        B = Ph;
+        h = hh + 1;
+      } else {  // back to its place: after every live key still larger
+        const int nk = ((mh - d) << 6) | (kh & (kWave - 1));
+        const int p = uni(hh + __popcll(ballot(lane > hh && key > nk) & live));
+        const bool mv = lane >= hh && lane < p;
+        const int ks = wave_shl1(key), us = wave_shl1(used), ps = wave_shl1(P);
+        key = mv ? ks : (lane == p ? nk : key);
+        used = mv ? us : (lane == p ? uh : used);
+        P = mv ? ps - mh : (lane >= p ? P - d : P);
       }
     }
-    if (exc > 0) return -1;
+    if (x > 0 && ++j < nm) {
+      if ((j & (kWave - 1)) == 0) load_experts(a, r, j, lane, s_eorder, s_elam, ev, lv);
+      continue;
+    }
+    fail = x > 0;
+    if (fail || ++oi >= R) break;
+    x = readlane(rk_l, oi) - tau;
+    if (x <= 0) break;
+    r = readlane(rk_r, oi);
+    load_experts(a, r, 0, lane, s_eorder, s_elam, ev, lv);
+    j = 0;
   }
-  const int base = n & ~(kWave - 1);
-  if (lane < (n & (kWave - 1))) {
-    s_re[base + lane] = cur_et;
-    s_rd[base + lane] = cur_d;
-  }
-  return n;
+  return fail ? -1 : n;
 }
 
 // The same probe for slacks of 25 bits or more: lane t holds rank t's slack
@@ -388,49 +471,73 @@ __device__ int probe_wide(const PlanArgs &a, int tau, int lane, int rk_r, int rk
   return n;
 }
 
-// Bisection state after rounds 0 .. upto: the state after the round before
-// (header slot, or the initial interval), then a walk of round `upto` over
-// its stored outcomes.
+// Bisection state before round rd: the initial interval, or the state
+// after round rd - 1 that round rd's first workgroup published.
 struct BisState {
   int64_t lo, hi;
   int best;   // last feasible probe: round * kNodes + node, or -1
   int probes; // probes of the sequential bisection so far
 };
 
-__device__ BisState state_after(const PlanArgs &a, int upto, int32_t *s_res, int lane) {
-  BisState st;
-  if (upto == 0) {
-    st = {a.ws.hdr[0], a.ws.hdr[1], -1, 0};
-  } else {
-    const int64_t *h = a.ws.hdr + 4 + 4 * (upto - 1);
-    st = {h[0], h[1], static_cast<int>(h[2]), static_cast<int>(h[3])};
+__device__ __forceinline__ BisState state_before(const PlanArgs &a, int rd) {
+  if (rd == 0) return {a.ws.hdr[0], a.ws.hdr[1], -1, 0};
+  const int64_t *h = a.ws.hdr + 4 + 4 * (rd - 1);
+  return {h[0], h[1], static_cast<int>(h[2]), static_cast<int>(h[3])};
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+  const uint32_t lo = static_cast<uint32_t>(readlane(static_cast<int>(v), l));
+  const uint32_t hi = static_cast<uint32_t>(readlane(static_cast<int>(v >> 32), l));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// The sequential bisection through round rd's depth-kDepth subtree, from
+// state st, over the round's outcome bits (word w in lane w).
+__device__ void walk_bits(uint64_t bw, int rd, BisState &st) {
+  int node = 0;
+  for (int d = 0; d < kDepth && st.lo < st.hi; ++d) {
+    const int64_t mid = (st.lo + st.hi) / 2;
+    ++st.probes;
+    const uint64_t w = readlane64(bw, node >> 6);
+    if ((w >> (node & 63)) & 1) {
+      st.hi = mid;
+      st.best = rd * kNodes + node;
+      node = 2 * node + 1;
+    } else {
+      st.lo = mid + 1;
+      node = 2 * node + 2;
+    }
   }
-  if (st.lo < st.hi) {
-    load_round(a.ws.res + upto * kNodes, s_res, lane);
-    __syncthreads();
-    int best = -1;
-    walk_round(s_res, st.lo, st.hi, best, st.probes);
-    if (best >= 0) st.best = upto * kNodes + best;
-  }
-  return st;
 }
 
 __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
-  __shared__ int32_t s_res[kNodes];
   __shared__ int32_t s_eorder[kMaxE];
   __shared__ int32_t s_elam[kMaxE];
   __shared__ uint32_t s_re[kMaxRec];
   __shared__ int32_t s_rd[kMaxRec];
   const int lane = threadIdx.x, b = blockIdx.x;
-  const int RS = a.R * a.NS;
-  if (a.ws.hdr[3] != 0) return;
-  int64_t lo, hi;
-  if (round == 0) {
-    lo = a.ws.hdr[0];
-    hi = a.ws.hdr[1];
-  } else {
-    // every workgroup walks the previous round; workgroup 0 publishes it
-    const BisState st = state_after(a, round - 1, s_res, lane);
+  const int R = a.R, E = a.E, RS = R * a.NS;
+  // every input is requested up front, so the round waits for memory once:
+  // the state before the previous round and that round's outcome bits, the
+  // per-rank expert orders and the rank orders
+  const int64_t status = a.ws.hdr[3];
+  const bool packed = a.ws.hdr[1] < (int64_t(1) << 25);
+  BisState st = state_before(a, round > 0 ? round - 1 : 0);
+  const uint64_t bw =
+      (round > 0 && lane < kBitWords) ? a.ws.bits[(round - 1) * kBitWords + lane] : 0;
+  int ve[kMaxE / kWave], vl[kMaxE / kWave];
+#pragma unroll
+  for (int u = 0; u < kMaxE / kWave; ++u) {
+    const int i = u * kWave + lane;
+    ve[u] = i < E ? a.ws.eorder[i] : 0;
+    vl[u] = i < E ? a.ws.elam[i] : 0;
+  }
+  const int rk_r = lane < R ? a.ws.rank_desc[lane] : 0;
+  const int as_r = lane < R ? a.ws.rank_asc[lane] : 0;
+  const int ell_lane = lane < R ? a.ws.ell[lane] : 0;
+  if (status != 0) return;
+  if (round > 0) {  // every workgroup walks the previous round; the first publishes it
+    walk_bits(bw, round - 1, st);
     if (b == 0 && lane == 0) {
       int64_t *h = a.ws.hdr + 4 + 4 * (round - 1);
       h[0] = st.lo;
@@ -438,11 +545,9 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
       h[2] = st.best;
       h[3] = st.probes;
     }
-    lo = st.lo;
-    hi = st.hi;
   }
+  int64_t lo = st.lo, hi = st.hi;
   if (lo >= hi) return;  // the bisection has ended
-  const bool packed = a.ws.hdr[1] < (int64_t(1) << 25);
   // this workgroup's node of the round's subtree
   const int id = b + 1, depth = 31 - __clz(id);
   bool reached = true;
@@ -455,37 +560,23 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
   int n = kNotReached;
   if (reached) {
     const int tau = static_cast<int>((lo + hi) / 2);
-    {  // stage the per-rank expert orders: up to 16 loads per lane in flight
-      for (int i0 = 0; i0 < a.E; i0 += 16 * kWave) {
-        int ve[16], vl[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int i = i0 + u * kWave + lane;
-          ve[u] = i < a.E ? a.ws.eorder[i] : 0;
-          vl[u] = i < a.E ? a.ws.elam[i] : 0;
-        }
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int i = i0 + u * kWave + lane;
-          if (i < a.E) {
-            s_eorder[i] = ve[u];
-            s_elam[i] = vl[u];
-          }
-        }
+    for (int u = 0; u < kMaxE / kWave; ++u) {
+      const int i = u * kWave + lane;
+      if (i < E) {
+        s_eorder[i] = ve[u];
+        s_elam[i] = vl[u];
       }
     }
-    const int rk_r = lane < a.R ? a.ws.rank_desc[lane] : 0;
-    const int as_r = lane < a.R ? a.ws.rank_asc[lane] : 0;
-    const int ell_lane = lane < a.R ? a.ws.ell[lane] : 0;
     const int rk_l = __shfl(ell_lane, rk_r);
     const int as_l = __shfl(ell_lane, as_r);
     __syncthreads();
     if (!packed)
       n = probe_wide(a, tau, lane, rk_r, rk_l, ell_lane, s_eorder, s_elam, s_re, s_rd);
     else if (a.NS == 1)
-      n = probe_sorted<true>(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
+      n = probe_one_slot(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
     else
-      n = probe_sorted<false>(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
+      n = probe_multi(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
     if (n > 0) {
       __syncthreads();
       uint32_t *rec = a.ws.rec + (static_cast<int64_t>(round) * kNodes + b) * 2 * RS;
@@ -495,13 +586,15 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
       }
     }
   }
-  if (lane == 0) a.ws.res[round * kNodes + b] = n;
+  if (lane == 0) {
+    a.ws.res[round * kNodes + b] = n;
+    if (n >= 0) atomicOr(a.ws.bits + round * kBitWords + (b >> 6), uint64_t(1) << (b & 63));
+  }
 }
 
 // ---------------------------------------------------------------- emit
 
 __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
-  __shared__ int32_t s_res[kNodes];
   __shared__ uint32_t s_et[kMaxRec];
   __shared__ int32_t s_d[kMaxRec];
   __shared__ int32_t s_ht[kMaxR];  // hosts of this expert: rank
@@ -509,12 +602,16 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   __shared__ int32_t s_fan[kMaxE];
   const int e = blockIdx.x, lane = threadIdx.x;
   const int R = a.R, E = a.E, NS = a.NS, nm = a.nm, ncol = a.ncol, RS = R * NS;
-  if (a.ws.hdr[3] != 0) {
-    if (e == 0 && lane < 8) a.stats[lane] = lane == 6 ? ULTRAEP_EDATA : (lane == 7 ? a.ws.hdr[2] : 0);
+  const int64_t status = a.ws.hdr[3], L = a.ws.hdr[2];
+  const int64_t lo0 = a.ws.hdr[0], hi0 = a.ws.hdr[1];
+  BisState fin = state_before(a, kRounds - 1);
+  const uint64_t bw = lane < kBitWords ? a.ws.bits[(kRounds - 1) * kBitWords + lane] : 0;
+  const int lam_e = a.ws.lam[e];
+  if (status != 0) {
+    if (e == 0 && lane < 8) a.stats[lane] = lane == 6 ? ULTRAEP_EDATA : (lane == 7 ? L : 0);
     return;
   }
-  const int64_t lo0 = a.ws.hdr[0], hi0 = a.ws.hdr[1];
-  const BisState fin = state_after(a, kRounds - 1, s_res, lane);
+  walk_bits(bw, kRounds - 1, fin);
   const int64_t hi = fin.hi;
   const int n_probe = fin.probes;
   const int best = fin.best;
@@ -528,7 +625,6 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   }
   __syncthreads();
   const int h = e / nm;
-  const int lam_e = a.ws.lam[e];
 
   // CSR row pointer: every expert has 1 + (its replicas) entries
   int before = 0, shed = 0;
@@ -612,54 +708,160 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
       a.stats[4] = nb;
       a.stats[5] = 1 + mf;
       a.stats[6] = 0;
-      a.stats[7] = a.ws.hdr[2];
+      a.stats[7] = L;
     }
   }
 }
 
 // ---------------------------------------------------------------- reroute
 
-// SolveReroute for expert blockIdx.x: hosts and quotas from the CSR lists
-// and U written by k_plan_emit, the expert's column of the load matrix.
-template <bool kExact, bool kOneRow>
-__device__ void split_expert(const PlanArgs &a, int e, int lane, int j0, int nh, int lam_r,
-                             int u_r, int t_i, int u_i) {
-  const int R = a.R, ncol = a.ncol;
-  // locality: a source that hosts e first consumes its own quota
-  const int loc_r = min(lam_r, u_r);
-  const int lamhat_r = lam_r - loc_r;
-  const int qloc_i = __shfl(loc_r, t_i);
-  int ures = lane < nh ? u_i - qloc_i : 0;
-  // residual quota total seen by source r: D_0 minus the demand of the
-  // sources before it; its reciprocal, all computed lane-parallel up front
-  int incl = lamhat_r;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(incl, o);
-    if (lane >= o) incl += t;
+// DPP wave_shr:1 - lane i receives lane i-1 (lane 0 keeps its value)
+__device__ __forceinline__ int wave_shr1(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x138, 0xF, 0xF, false);
+}
+
+// Two hosts (home first, one replica): with residual quotas (u0, u1) and
+// residual demand D = u0 + u1, a source with demand lh gives host 0
+// b0 = floor(lh * u0 / D) plus the one leftover unit when its remainder is
+// at least the other host's (ties go to the earlier host), i.e.
+// q0 = floor((lh * u0 + D / 2) / D).  The sources run in ascending order with
+// the state u0 carried from lane r to lane r + 1 by a DPP shift, so the chain
+// has no scalar round trip and no branch.  Lane r returns q0 of source r.
+//   kExact: lh * u0 + D / 2 < 2^52 (total load below 2^26), so the fp64
+//   numerator is exact and one correction of the reciprocal estimate
+//   gives the floor; otherwise the same in int64.
+template <bool kExact>
+__device__ int split_two(int lamhat, int Dr, int u0_init, int R) {
+  const bool act = lamhat > 0;
+  const double lhd = static_cast<double>(lamhat);
+  const double Dd = act ? static_cast<double>(Dr) : 1.0;
+  const double rD = 1.0 / Dd;
+  const double half = 0.5 * Dd;
+  int u0 = u0_init, qout = 0;
+  const int lane = lane_id();
+  for (int r = 0; r < R; ++r) {
+    int q;
+    if (kExact) {
+      const double N = __builtin_fma(lhd, static_cast<double>(u0), half);
+      const double t = __builtin_trunc(N * rD);
+      const double rr = __builtin_fma(-t, Dd, N);
+      q = static_cast<int>(t) + (rr >= Dd ? 1 : 0) - (rr < 0.0 ? 1 : 0);
+    } else {
+      const int64_t D = act ? Dr : 1;
+      const int64_t N = 2 * static_cast<int64_t>(lamhat) * u0 + D;
+      int64_t t = static_cast<int64_t>(static_cast<double>(N) * (0.5 * rD));
+      const int64_t rr = N - t * 2 * D;
+      t += (rr >= 2 * D ? 1 : 0) - (rr < 0 ? 1 : 0);
+      q = static_cast<int>(t);
+    }
+    qout = lane == r ? q : qout;
+    u0 = wave_shr1(u0 - q);
   }
-  const int D0 = wave_sum(ures);
-  const int Dr = D0 - (incl - lamhat_r);
+  return qout;
+}
+
+// A few hosts (NH of them, home first): the same chain as split_two with
+// the residual quotas of hosts 0 .. NH-2 carried from lane r to lane r + 1;
+// the last host's quota is the rest of the residual demand.  Each source
+// computes the floor and remainder of lh * u_i / D for those hosts side by
+// side; for the last host they follow from the sum S of the others'
+// remainders, since all remainders add up to (leftover units) * D:
+// leftover = ceil(S / D) and its remainder is leftover * D - S.  The
+// leftover units go to the largest remainders (ties to the earlier host).
+// Needs lh * u below 2^52 (total load below 2^26).  Lane r returns source
+// r's share for each host in q[].
+template <int NH>
+__device__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH]) {
+  const bool act = lamhat > 0;
+  const double lhd = static_cast<double>(lamhat);
+  const int Di = act ? Dr : 1;
+  const double Dd = static_cast<double>(Di);
+  const double rD = 1.0 / Dd;
+  const int lane = lane_id();
+#pragma unroll
+  for (int i = 0; i < NH; ++i) q[i] = 0;
+  for (int r = 0; r < R; ++r) {
+    int b[NH], rem[NH];
+    int sb = 0, srem = 0;
+#pragma unroll
+    for (int i = 0; i < NH - 1; ++i) {
+      const double pr = lhd * static_cast<double>(u[i]);
+      const double t = __builtin_trunc(pr * rD);
+      const double rr = __builtin_fma(-t, Dd, pr);
+      const int lo = rr < 0.0 ? 1 : 0, hi = rr >= Dd ? 1 : 0;
+      b[i] = static_cast<int>(t) + hi - lo;
+      rem[i] = static_cast<int>(rr) + (lo ? Di : 0) - (hi ? Di : 0);
+      sb += b[i];
+      srem += rem[i];
+    }
+    // srem < (NH - 1) * D: leftover = ceil(srem / D), at most NH - 1
+    int left = 0;
+#pragma unroll
+    for (int k = 1; k < NH; ++k) left += srem > (k - 1) * Di ? 1 : 0;
+    rem[NH - 1] = left * Di - srem;
+    b[NH - 1] = lamhat - sb - left;
+    const bool me = lane == r;
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      int rk = 0;  // hosts ahead of i in (remainder descending, host ascending)
+#pragma unroll
+      for (int k = 0; k < NH; ++k)
+        if (k != i) rk += k < i ? (rem[k] >= rem[i] ? 1 : 0) : (rem[k] > rem[i] ? 1 : 0);
+      const int qi = b[i] + (rk < left ? 1 : 0);
+      q[i] = me ? qi : q[i];
+      if (i < NH - 1) u[i] = wave_shr1(u[i] - qi);
+    }
+  }
+}
+
+// Runs split_small for NH hosts: hosts' ranks t[] and residual quotas come
+// from the replica mask; writes rows of Q (lane = source rank).
+template <int NH>
+__device__ void reroute_small(int h, uint64_t rep, int lamhat_r, int Dr, int ures_r,
+                              int loc_r, int R, int32_t *qrow, int j0) {
+  const int lane = lane_id();
+  int t[NH], u[NH], q[NH];
+  t[0] = h;
+  uint64_t mrest = rep;
+#pragma unroll
+  for (int i = 1; i < NH; ++i) {
+    t[i] = __ffsll(static_cast<unsigned long long>(mrest)) - 1;
+    mrest &= mrest - 1;
+  }
+#pragma unroll
+  for (int i = 0; i < NH; ++i) u[i] = readlane(ures_r, t[i]);
+  split_small<NH>(lamhat_r, Dr, u, R, q);
+  if (lane < R) {
+#pragma unroll
+    for (int i = 0; i < NH; ++i) qrow[j0 + i] = q[i] + (lane == t[i] ? loc_r : 0);
+  }
+}
+
+// Any number of hosts: lane i is host i (home first, then replicas by
+// ascending rank) with residual quota ures; the sources run in ascending
+// order, each splitting its residual demand by largest remainder.  Writes
+// q of source r, host `lane` to qcol[r * ncol].
+template <bool kExact, bool kOneRow>
+__device__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int R,
+                           int64_t ncol, int32_t *qcol, int t_i, int qloc_i) {
   const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
-  int32_t *qcol = a.q + j0 + lane;
+  const bool host = lane < nh;
   for (int r = 0; r < R; ++r) {
     const int lh = readlane(lamhat_r, r);
     int qi = 0;
     if (lh > 0) {
       const int D = readlane(Dr, r);
       const double rD = readlane_d(rDr, r);
-      // floor(lh * ures / D): fp64 estimate (far below one unit off since
-      // the quotient is < 2^30), made exact by one correction
+      // floor(lh * ures / D) and its remainder, exact after one correction
       int b, rem;
-      if (kExact) {  // all operands below 2^26: products below 2^52, exact
+      if (kExact) {  // lh * ures < 2^52
         const double Dd = static_cast<double>(D);
         const double pr = static_cast<double>(lh) * static_cast<double>(ures);
-        double bq = __builtin_trunc(pr * rD);
-        double rd = __builtin_fma(-bq, Dd, pr);
-        const bool lo = rd < 0.0, hi = rd >= Dd;
-        bq += lo ? -1.0 : (hi ? 1.0 : 0.0);
-        rd += lo ? Dd : (hi ? -Dd : 0.0);
-        b = static_cast<int>(bq);
-        rem = static_cast<int>(rd);
+        const double bq = __builtin_trunc(pr * rD);
+        const double rd = __builtin_fma(-bq, Dd, pr);
+        const int lo = rd < 0.0 ? 1 : 0, hi = rd >= Dd ? 1 : 0;
+        b = static_cast<int>(bq) + hi - lo;
+        rem = static_cast<int>(rd) + (lo ? D : 0) - (hi ? D : 0);
       } else {
         b = static_cast<int>(static_cast<double>(lh) * static_cast<double>(ures) * rD);
         int64_t rm = static_cast<int64_t>(lh) * ures - static_cast<int64_t>(b) * D;
@@ -669,43 +871,94 @@ __device__ void split_expert(const PlanArgs &a, int e, int lane, int j0, int nh,
         rem = static_cast<int>(rm);
       }
       const int left = lh - (kOneRow ? readlane(row_sum(b), 0) : wave_sum(b));
-      int extra = 0;
-      if (left > 0) {  // the `left` hosts with the largest remainders
-        int rk = 0;
-        for (int j = 0; j < nh; ++j) {
-          const int rj = readlane(rem, j);
-          rk += (rj > rem) || (rj == rem && j < lane);
-        }
-        extra = (lane < nh && rk < left) ? 1 : 0;
+      // the `left` hosts with the largest remainders (ties: earlier host)
+      int rk = 0;
+      for (int j = 0; j < nh; ++j) {
+        const int rj = readlane(rem, j);
+        rk += (rj > rem) || (rj == rem && j < lane);
       }
-      qi = b + extra;
+      qi = b + ((host && rk < left) ? 1 : 0);
       ures -= qi;
     }
-    if (lane < nh) qcol[static_cast<int64_t>(r) * ncol] = qi + (t_i == r ? qloc_i : 0);
+    if (host) qcol[r * ncol] = qi + (t_i == r ? qloc_i : 0);
   }
 }
 
+// SolveReroute for expert blockIdx.x (one wave).  The hosts of e are its
+// home and every other rank with a positive quota (a replica's quota is at
+// least u_min), so U's row, the load column and the expert's first CSR
+// column are all the inputs, loaded together.  Locality first: a host
+// consumes its own tokens up to its quota; the residual demands are then
+// split over the residual quotas.
 __global__ void __launch_bounds__(kWave) k_plan_reroute(PlanArgs a) {
+  __shared__ int32_t s_t[kWave];
   const int e = blockIdx.x, lane = threadIdx.x;
-  const int R = a.R, E = a.E, ncol = a.ncol;
-  if (a.stats[6] != 0) return;
-  const int j0 = a.hp[e], nh = a.hp[e + 1] - j0, total = a.hp[E];
+  const int R = a.R, E = a.E;
+  const int64_t ncol = a.ncol;
+  const int h = e / a.nm;
+  const int64_t status = a.stats[6], L = a.stats[7];
+  const int j0 = a.hp[e], total = a.hp[E];
   const int lam_r = lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
+  const int u_r = lane < R ? a.U[static_cast<int64_t>(e) * R + lane] : 0;
+  if (status != 0) return;
+  const uint64_t rep = ballot(lane < R && lane != h && u_r > 0);
+  const int nh = 1 + __popcll(rep);
+  if (j0 < e || j0 + nh > total || total > ncol) {  // not a plan of this group
+    if (lane == 0) a.stats[6] = ULTRAEP_EDATA;
+    return;
+  }
+  const int loc_r = min(lam_r, u_r);  // 0 on ranks that do not host e
+  const int lamhat_r = lam_r - loc_r;
+  const int ures_r = u_r - loc_r;
+  // residual demand still to place when source r comes: D0 minus the
+  // demand of the sources before it
+  int incl = lamhat_r;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  const int D0 = readlane(incl, kWave - 1);
+  const int Dr = D0 - (incl - lamhat_r);
+  const bool exact = L < (int64_t(1) << 26);
+  int32_t *qrow = a.q + static_cast<int64_t>(lane) * ncol;
   if (nh == 1) {
-    if (lane < R) a.q[static_cast<int64_t>(lane) * ncol + j0] = lam_r;
+    if (lane < R) qrow[j0] = lam_r;
+  } else if (nh == 2) {
+    const int t = __ffsll(static_cast<unsigned long long>(rep)) - 1;
+    const int u0 = readlane(ures_r, h);
+    const int q0 = exact ? split_two<true>(lamhat_r, Dr, u0, R)
+                         : split_two<false>(lamhat_r, Dr, u0, R);
+    if (lane < R) {
+      qrow[j0] = q0 + (lane == h ? loc_r : 0);
+      qrow[j0 + 1] = lamhat_r - q0 + (lane == t ? loc_r : 0);
+    }
+  } else if (exact && nh == 3) {
+    reroute_small<3>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
+  } else if (exact && nh == 4) {
+    reroute_small<4>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
   } else {
-    const int u_r = lane < R ? a.U[static_cast<int64_t>(e) * R + lane] : 0;
-    const int t_i = lane < nh ? a.hr[j0 + lane] : 0;
-    const int u_i = __shfl(u_r, t_i);
-    const bool exact = a.stats[7] < (int64_t(1) << 26);
-    if (exact && nh <= 16) split_expert<true, true>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
-    else if (exact) split_expert<true, false>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
-    else if (nh <= 16) split_expert<false, true>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
-    else split_expert<false, false>(a, e, lane, j0, nh, lam_r, u_r, t_i, u_i);
+    if (lane == h) s_t[0] = h;
+    if ((rep >> lane) & 1) s_t[1 + popc_below(rep)] = lane;
+    __syncthreads();
+    const int t_i = lane < nh ? s_t[lane] : 0;
+    // every lane takes part in the shuffles: a lane reads only from lanes
+    // that execute the same shuffle
+    const int ures_t = __shfl(ures_r, t_i);
+    const int qloc_i = __shfl(loc_r, t_i);
+    const int ures_i = lane < nh ? ures_t : 0;
+    int32_t *qcol = a.q + j0 + lane;
+    if (exact && nh <= 16)
+      split_many<true, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (exact)
+      split_many<true, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (nh <= 16)
+      split_many<false, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else
+      split_many<false, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
   }
   // CSR padding columns of Q
   for (int j = total + e; j < ncol; j += E)
-    for (int r = lane; r < R; r += kWave) a.q[static_cast<int64_t>(r) * ncol + j] = 0;
+    if (lane < R) qrow[j] = 0;
 }
 
 static PlanArgs plan_args(const int32_t *load, const ultraep_group &g,
