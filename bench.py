@@ -3,8 +3,7 @@
 
 One step = one layer-microbatch of the hot path on the measured rank:
   count      (that rank's top-k ids -> its row of the load matrix)
-  replicate  (SolveReplication over the whole EP group)
-  reroute    (SolveReroute)
+  plan       (SolveReplication then SolveReroute over the whole EP group)
   dispatch   layout + row scatter (bf16 rows into per-replica send blocks)
   pack       (replicated main-expert blobs into per-destination staging)
 on synthetic DeepSeek-V3-shaped training routing (E=256, top-8 with
@@ -13,14 +12,15 @@ on synthetic DeepSeek-V3-shaped training routing (E=256, top-8 with
 resident inputs (the all-gather that delivers them is not on one GPU).  The
 measured rank is the one with the most outbound replica bytes.
 
-Timed region: K replays of the step captured in one HIP graph, bracketed by
-device synchronisation.  Inside the graph the step follows the forward
-pipeline of Eq. (1): once SolveReplication is done, the weight packing runs
-on a second stream while reroute, layout and scatter run on the first; the
-two join at the end of the step.  The graph's outputs are checked against a
-sequential eager step.  A second pass of K sequential eager steps records
-HIP events around every launch on the launch stream; the dominant kernel's
-average duration gives the roofline figures.  The CPU oracle is timed
+Timed region: K replays of the step captured in one HIP graph on one
+stream, bracketed by device synchronisation.  (Running the packing on a
+second stream next to reroute and dispatch, as the forward pipeline of
+Eq. (1) allows, measured slower on one GPU: the cross-queue dependencies of
+the graph cost more than the overlap gains, and the packing's workgroups
+crowd out the latency-bound kernels.)  The graph's outputs are checked
+against an eager step.  A second pass of K eager steps records HIP events
+around every launch on the launch stream; the dominant kernel's average
+duration gives the roofline figures.  The CPU oracle is timed
 single-threaded on a bounded sample of the same workload.
 
 Prints one JSON line.
@@ -123,8 +123,7 @@ def main():
 
     calls = [
         ("count", lambda: uep.ultraep_count(topk_r, T, k, c.E, 1, load_r, status)),
-        ("plan_replicate", lambda: uep.ultraep_plan_replicate(load, g, plan)),
-        ("plan_reroute", lambda: uep.ultraep_plan_reroute(load, g, plan)),
+        ("plan", lambda: uep.ultraep_plan(load, g, plan)),
         ("dispatch_layout", lambda: uep.ultraep_dispatch_layout(
             topk_r, T, k, rank, g, plan, ros, boff, ws, status)),
         ("dispatch_scatter", lambda: uep.ultraep_dispatch_scatter(
@@ -132,23 +131,10 @@ def main():
         ("pack", lambda: uep.ultraep_pack_replicas(
             w, W, rank, g, plan, staging, cap, doff, status)),
     ]
-    fn = dict(calls)
-    side = torch.cuda.Stream()  # default priority
 
     def step():
         for _, f in calls:
             f()
-
-    def step_overlapped():
-        fn["count"]()
-        fn["plan_replicate"]()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            fn["pack"]()  # needs only the replica placement
-        fn["plan_reroute"]()
-        fn["dispatch_layout"]()
-        fn["dispatch_scatter"]()
-        torch.cuda.current_stream().wait_stream(side)
 
     outputs = (load_r, send, ros, boff, staging, doff,
                *[getattr(plan, f) for f in uep.PLAN_FIELDS])
@@ -162,11 +148,11 @@ def main():
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
-        step_overlapped()
+        step()
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     with torch.cuda.graph(graph):
-        step_overlapped()
+        step()
     for t in outputs:
         t.fill_(-1)
     for _ in range(max(1, args.warmup)):
@@ -255,8 +241,7 @@ def main():
             "routed_rows": n_routed,
             "replicas_shipped": int(n_out_r[rank]),
             "expert_blob_bytes": W_bytes,
-            "timed": ("HIP graph replay of count, replicate, then "
-                      "{reroute, layout, scatter} alongside {pack}"),
+            "timed": "HIP graph replay of count, plan, dispatch layout, scatter, pack",
         },
         "roofline": {
             "kernel": dom,
@@ -270,8 +255,7 @@ def main():
             "avg_launch_us": round(dus, 2),
         },
         "kernels_us": {n: round(v, 2) for n, v in per_call_us.items()},
-        "count_plan_us": round(per_call_us["count"] + per_call_us["plan_replicate"]
-                               + per_call_us["plan_reroute"], 2),
+        "count_plan_us": round(per_call_us["count"] + per_call_us["plan"], 2),
         "eager_us_per_step": round(t_eager * 1e6, 2),
         "dispatch_scatter_GBps": round(scatter_bytes / per_call_us["dispatch_scatter"] / 1e3, 1),
         "pack_GBps": round(pack_bytes / per_call_us["pack"] / 1e3, 1) if pack_bytes else None,

@@ -81,8 +81,9 @@ int ultraep_plan_reroute(const int32_t *load, const ultraep_group *g,
 int ultraep_plan(const int32_t *load, const ultraep_group *g,
                  const ultraep_plan_buf *out, void *ws, size_t ws_bytes,
                  hipStream_t stream) {
-  const int r = ultraep_plan_replicate(load, g, out, ws, ws_bytes, stream);
-  return r != ULTRAEP_OK ? r : ultraep_plan_reroute(load, g, out, stream);
+  if (!load || !group_ok(g) || !plan_ok(g, out) || !ws) return ULTRAEP_EINVAL;
+  if (ws_bytes < uep::plan_ws_bytes(g->R, g->E, g->n_slot)) return ULTRAEP_EINVAL;
+  return rc(uep::launch_plan(load, *g, *out, ws, stream));
 }
 
 size_t ultraep_dispatch_ws_bytes(int64_t T, int32_t k, const ultraep_group *g) {

@@ -18,6 +18,9 @@ hipError_t launch_plan_replicate(const int32_t *load, const ultraep_group &g,
                                  const ultraep_plan_buf &out, void *ws, hipStream_t stream);
 hipError_t launch_plan_reroute(const int32_t *load, const ultraep_group &g,
                                const ultraep_plan_buf &out, hipStream_t stream);
+// both halves, the reroute fused into the last kernel of the replication
+hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
+                       const ultraep_plan_buf &out, void *ws, hipStream_t stream);
 
 // dispatch workspace carve-up
 struct DispatchWs {

@@ -3,14 +3,17 @@
 // of that expert's blob, in per-destination staging ordered by destination
 // rank, then slot.
 //
-// One kernel with a persistent grid.  Each workgroup first derives the task
-// list from the slot map in LDS (at most R * n_slot entries): the entry index
-// of every destination, the replicated local experts and, per expert, its
-// destination entries.  Workgroup 0 also writes dest_off.  The copy then
-// walks tasks (expert, 32 KiB tile) with a grid stride, experts interleaved
-// so hot and cold experts spread over all workgroups: each tile is loaded
-// once into registers with 16-byte loads and stored to every destination
-// with 16-byte non-temporal stores, so every source byte is read once.
+// One kernel with a grid-stride loop over (expert, 16 KiB tile) tasks.  Each
+// workgroup first derives the tasks from the slot map in LDS (at most
+// R * n_slot entries): a slot's staging entry is the number of this rank's
+// replicas in earlier slots (a ballot prefix), and the entries are grouped
+// by local expert with LDS counters (every destination of an expert gets the
+// whole blob, so the order inside a group does not matter; the groups are
+// numbered by ascending local expert in every workgroup).  Workgroup 0
+// also writes dest_off.  Each tile is loaded once into registers with
+// 16-byte loads and stored to every destination of its expert with 16-byte
+// non-temporal stores, so every source byte is read once; the experts
+// interleave so hot and cold ones spread over all workgroups.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -18,10 +21,11 @@ namespace uep {
 
 constexpr int kPkThreads = 256;
 constexpr int kPkWaves = kPkThreads / kWave;
-constexpr int kPkUnroll = 8;                        // v4u per thread per tile
-constexpr int kPkTileCh = kPkThreads * kPkUnroll;   // 2048 x 16 B = 32 KiB
+constexpr int kPkUnroll = 4;                        // v4u per thread per tile
+constexpr int kPkTileCh = kPkThreads * kPkUnroll;   // 1024 x 16 B = 16 KiB
 constexpr int kPkMaxEnt = 256;                      // R * n_slot
-constexpr int kPkGrid = 2048;
+constexpr int kPkMaxLocal = 1024;                   // main experts per rank
+constexpr int kPkGrid = 4096;  // about one tile per workgroup at these sizes
 
 struct PkArgs {
   const v4u *w;
@@ -35,15 +39,16 @@ struct PkArgs {
 };
 
 __global__ void __launch_bounds__(kPkThreads) k_pack(PkArgs a) {
-  __shared__ int32_t s_li[kPkMaxEnt];     // local expert of slot j, or -1
-  __shared__ int32_t s_sorted[kPkMaxEnt]; // entries grouped by local expert
-  __shared__ int32_t s_gli[kPkMaxEnt], s_gstart[kPkMaxEnt], s_gfan[kPkMaxEnt];
-  __shared__ int32_t s_first[kPkMaxEnt];
-  __shared__ int32_t s_wcnt[kPkWaves + 1];
-  __shared__ int32_t s_ngrp;
+  __shared__ int32_t s_dst[kPkMaxEnt];         // destination entries, grouped by expert
+  __shared__ int32_t s_cnt[kPkMaxLocal];       // per local expert: destinations
+  __shared__ int32_t s_gstart[kPkMaxLocal];    //                   first s_dst index
+  __shared__ int32_t s_gli[kPkMaxEnt];         // per group: local expert
+  __shared__ int32_t s_wcnt[kPkWaves];
+  __shared__ int32_t s_ngrp, s_off;
 
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int RS = a.R * a.NS;
+  for (int l = tid; l < a.nm; l += kPkThreads) s_cnt[l] = 0;
   int li = -1;
   if (tid < RS) {
     const int e = a.X[tid];
@@ -52,19 +57,24 @@ __global__ void __launch_bounds__(kPkThreads) k_pack(PkArgs a) {
   const bool valid = li >= 0;
   const uint64_t bv = ballot(valid);
   if (lane == 0) s_wcnt[wave] = __popcll(bv);
-  s_li[tid] = li;
-  if (tid == 0) s_ngrp = 0;
+  if (tid == 0) {
+    s_ngrp = 0;
+    s_off = 0;
+  }
   __syncthreads();
-  int before = popc_below(bv);
-  for (int w = 0; w < wave; ++w) before += s_wcnt[w];
-  int n_out = 0;
-  for (int w = 0; w < kPkWaves; ++w) n_out += s_wcnt[w];
-
+  // staging entry of this slot: valid slots before it (destination rank
+  // ascending, then slot)
+  int entry = popc_below(bv), n_out = 0;
+  for (int w = 0; w < kPkWaves; ++w) {
+    entry += w < wave ? s_wcnt[w] : 0;
+    n_out += s_wcnt[w];
+  }
   if (blockIdx.x == 0) {
-    for (int t = tid; t <= a.R; t += kPkThreads) {
-      int c = 0;
-      for (int j = 0; j < t * a.NS; ++j) c += s_li[j] >= 0;
-      a.dest_off[t] = c;
+    if (a.NS == 0) {
+      for (int t = tid; t <= a.R; t += kPkThreads) a.dest_off[t] = 0;
+    } else {
+      if (tid < RS && tid % a.NS == 0) a.dest_off[tid / a.NS] = entry;
+      if (tid == 0) a.dest_off[a.R] = n_out;
     }
   }
   if (n_out > a.cap) {
@@ -72,44 +82,48 @@ __global__ void __launch_bounds__(kPkThreads) k_pack(PkArgs a) {
     return;
   }
   if (n_out == 0) return;
-  int fidx = 0, smaller = 0, fan = 0;
-  if (valid) {
-    for (int j = 0; j < RS; ++j) {
-      const int lj = s_li[j];
-      if (lj < 0) continue;
-      fidx += (lj == li) && (j < tid);
-      fan += lj == li;
-      smaller += lj < li;
-    }
-    s_sorted[smaller + fidx] = before;
-  }
-  s_first[tid] = valid && fidx == 0;
+  // group the entries by local expert: every destination of an expert gets
+  // the whole blob, so the order inside a group is free
+  const int fidx = valid ? atomicAdd(&s_cnt[li], 1) : -1;
   __syncthreads();
-  if (valid && fidx == 0) {
-    int grp = 0;  // replicated local experts with a smaller index
-    for (int j = 0; j < RS; ++j) grp += s_first[j] && s_li[j] < li;
-    s_gli[grp] = li;
-    s_gstart[grp] = smaller;
-    s_gfan[grp] = fan;
-    atomicAdd(&s_ngrp, 1);
+  if (fidx == 0) s_gstart[li] = atomicAdd(&s_off, s_cnt[li]);
+  // the groups themselves in ascending local-expert order, the same in
+  // every workgroup, since tasks are numbered by group
+  for (int l0 = 0; l0 < a.nm; l0 += kPkThreads) {
+    const int l = l0 + tid;
+    const bool has = l < a.nm && s_cnt[l] > 0;
+    const uint64_t hb = ballot(has);
+    int gi = s_ngrp + popc_below(hb);
+    __syncthreads();
+    if (lane == 0) s_wcnt[wave] = __popcll(hb);
+    __syncthreads();
+    int tot = 0;
+    for (int w = 0; w < kPkWaves; ++w) {
+      gi += w < wave ? s_wcnt[w] : 0;
+      tot += s_wcnt[w];
+    }
+    if (has) s_gli[gi] = l;
+    __syncthreads();
+    if (tid == 0) s_ngrp += tot;
   }
+  if (valid) s_dst[s_gstart[li] + fidx] = entry;
   __syncthreads();
   const int ngrp = s_ngrp;
   const int64_t ntile = (a.nch + kPkTileCh - 1) / kPkTileCh;
   const int64_t ntask = ntile * ngrp;
   for (int64_t task = blockIdx.x; task < ntask; task += gridDim.x) {
-    const int g = static_cast<int>(task % ngrp);
+    const int l = s_gli[static_cast<int>(task % ngrp)];
     const int64_t c0 = (task / ngrp) * kPkTileCh;
-    const v4u *src = a.w + static_cast<int64_t>(s_gli[g]) * a.nch;
+    const v4u *src = a.w + static_cast<int64_t>(l) * a.nch;
     v4u v[kPkUnroll];
 #pragma unroll
     for (int u = 0; u < kPkUnroll; ++u) {
       const int64_t c = c0 + u * kPkThreads + tid;
       if (c < a.nch) v[u] = __builtin_nontemporal_load(src + c);
     }
-    const int fan = s_gfan[g], st = s_gstart[g];
+    const int fan = s_cnt[l], st = s_gstart[l];
     for (int f = 0; f < fan; ++f) {
-      v4u *dst = a.staging + static_cast<int64_t>(s_sorted[st + f]) * a.nch;
+      v4u *dst = a.staging + static_cast<int64_t>(s_dst[st + f]) * a.nch;
 #pragma unroll
       for (int u = 0; u < kPkUnroll; ++u) {
         const int64_t c = c0 + u * kPkThreads + tid;

@@ -592,9 +592,258 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
   }
 }
 
+// ---------------------------------------------------------------- reroute
+
+// DPP wave_shr:1 - lane i receives lane i-1 (lane 0 keeps its value)
+__device__ __forceinline__ int wave_shr1(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x138, 0xF, 0xF, false);
+}
+
+// Two hosts (home first, one replica): with residual quotas (u0, u1) and
+// residual demand D = u0 + u1, a source with demand lh gives host 0
+// b0 = floor(lh * u0 / D) plus the one leftover unit when its remainder is
+// at least the other host's (ties go to the earlier host), i.e.
+// q0 = floor((lh * u0 + D / 2) / D).  The sources run in ascending order with
+// the state u0 carried from lane r to lane r + 1 by a DPP shift, so the chain
+// has no scalar round trip and no branch.  Lane r returns q0 of source r.
+//   kExact: lh * u0 + D / 2 < 2^52 (total load below 2^26), so the fp64
+//   numerator is exact and one correction of the reciprocal estimate
+//   gives the floor; otherwise the same in int64.
+template <bool kExact>
+__device__ int split_two(int lamhat, int Dr, int u0_init, int R) {
+  const bool act = lamhat > 0;
+  const double lhd = static_cast<double>(lamhat);
+  const double Dd = act ? static_cast<double>(Dr) : 1.0;
+  const double rD = 1.0 / Dd;
+  const double half = 0.5 * Dd;
+  int u0 = u0_init, qout = 0;
+  const int lane = lane_id();
+  for (int r = 0; r < R; ++r) {
+    int q;
+    if (kExact) {
+      const double N = __builtin_fma(lhd, static_cast<double>(u0), half);
+      const double t = __builtin_trunc(N * rD);
+      const double rr = __builtin_fma(-t, Dd, N);
+      q = static_cast<int>(t) + (rr >= Dd ? 1 : 0) - (rr < 0.0 ? 1 : 0);
+    } else {
+      const int64_t D = act ? Dr : 1;
+      const int64_t N = 2 * static_cast<int64_t>(lamhat) * u0 + D;
+      int64_t t = static_cast<int64_t>(static_cast<double>(N) * (0.5 * rD));
+      const int64_t rr = N - t * 2 * D;
+      t += (rr >= 2 * D ? 1 : 0) - (rr < 0 ? 1 : 0);
+      q = static_cast<int>(t);
+    }
+    qout = lane == r ? q : qout;
+    u0 = wave_shr1(u0 - q);
+  }
+  return qout;
+}
+
+// A few hosts (NH of them, home first): the same chain as split_two with
+// the residual quotas of hosts 0 .. NH-2 carried from lane r to lane r + 1;
+// the last host's quota is the rest of the residual demand.  Each source
+// computes the floor and remainder of lh * u_i / D for those hosts side by
+// side; for the last host they follow from the sum S of the others'
+// remainders, since all remainders add up to (leftover units) * D:
+// leftover = ceil(S / D) and its remainder is leftover * D - S.  The
+// leftover units go to the largest remainders (ties to the earlier host).
+// Needs lh * u below 2^52 (total load below 2^26).  Lane r returns source
+// r's share for each host in q[].
+template <int NH>
+__device__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH]) {
+  const bool act = lamhat > 0;
+  const double lhd = static_cast<double>(lamhat);
+  const int Di = act ? Dr : 1;
+  const double rD = 1.0 / static_cast<double>(Di);
+  const int lane = lane_id();
+#pragma unroll
+  for (int i = 0; i < NH; ++i) q[i] = 0;
+  for (int r = 0; r < R; ++r) {
+    int b[NH], rem[NH];
+    int sb = 0, srem = 0;
+#pragma unroll
+    for (int i = 0; i < NH - 1; ++i) {
+      // floor(lh * u / D) within one from the fp64 estimate (the product
+      // is exact); the remainder for that estimate lies in (-D, 2D), so
+      // wrapping 32-bit arithmetic gives it exactly
+      const int bi = static_cast<int>(lhd * static_cast<double>(u[i]) * rD);
+      const int ri = static_cast<int>(static_cast<uint32_t>(lamhat) * static_cast<uint32_t>(u[i]) -
+                                      static_cast<uint32_t>(bi) * static_cast<uint32_t>(Di));
+      const int lo = ri < 0 ? 1 : 0, hi = ri >= Di ? 1 : 0;
+      b[i] = bi + hi - lo;
+      rem[i] = ri + (lo ? Di : 0) - (hi ? Di : 0);
+      sb += b[i];
+      srem += rem[i];
+    }
+    // srem < (NH - 1) * D: leftover = ceil(srem / D), at most NH - 1
+    int left = 0;
+#pragma unroll
+    for (int k = 1; k < NH; ++k) left += srem > (k - 1) * Di ? 1 : 0;
+    rem[NH - 1] = left * Di - srem;
+    b[NH - 1] = lamhat - sb - left;
+    const bool me = lane == r;
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      int rk = 0;  // hosts ahead of i in (remainder descending, host ascending)
+#pragma unroll
+      for (int k = 0; k < NH; ++k)
+        if (k != i) rk += k < i ? (rem[k] >= rem[i] ? 1 : 0) : (rem[k] > rem[i] ? 1 : 0);
+      const int qi = b[i] + (rk < left ? 1 : 0);
+      q[i] = me ? qi : q[i];
+      if (i < NH - 1) u[i] = wave_shr1(u[i] - qi);
+    }
+  }
+}
+
+// Runs split_small for NH hosts: hosts' ranks t[] and residual quotas come
+// from the replica mask; writes rows of Q (lane = source rank).
+template <int NH>
+__device__ void reroute_small(int h, uint64_t rep, int lamhat_r, int Dr, int ures_r,
+                              int loc_r, int R, int32_t *qrow, int j0) {
+  const int lane = lane_id();
+  int t[NH], u[NH], q[NH];
+  t[0] = h;
+  uint64_t mrest = rep;
+#pragma unroll
+  for (int i = 1; i < NH; ++i) {
+    t[i] = __ffsll(static_cast<unsigned long long>(mrest)) - 1;
+    mrest &= mrest - 1;
+  }
+#pragma unroll
+  for (int i = 0; i < NH; ++i) u[i] = readlane(ures_r, t[i]);
+  split_small<NH>(lamhat_r, Dr, u, R, q);
+  if (lane < R) {
+#pragma unroll
+    for (int i = 0; i < NH; ++i) qrow[j0 + i] = q[i] + (lane == t[i] ? loc_r : 0);
+  }
+}
+
+// Any number of hosts: lane i is host i (home first, then replicas by
+// ascending rank) with residual quota ures; the sources run in ascending
+// order, each splitting its residual demand by largest remainder.  Writes
+// q of source r, host `lane` to qcol[r * ncol].
+template <bool kExact, bool kOneRow>
+__device__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int R,
+                           int64_t ncol, int32_t *qcol, int t_i, int qloc_i) {
+  const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
+  const bool host = lane < nh;
+  for (int r = 0; r < R; ++r) {
+    const int lh = readlane(lamhat_r, r);
+    int qi = 0;
+    if (lh > 0) {
+      const int D = readlane(Dr, r);
+      const double rD = readlane_d(rDr, r);
+      // floor(lh * ures / D) and its remainder, exact after one correction
+      int b, rem;
+      if (kExact) {  // lh * ures < 2^52
+        const double Dd = static_cast<double>(D);
+        const double pr = static_cast<double>(lh) * static_cast<double>(ures);
+        const double bq = __builtin_trunc(pr * rD);
+        const double rd = __builtin_fma(-bq, Dd, pr);
+        const int lo = rd < 0.0 ? 1 : 0, hi = rd >= Dd ? 1 : 0;
+        b = static_cast<int>(bq) + hi - lo;
+        rem = static_cast<int>(rd) + (lo ? D : 0) - (hi ? D : 0);
+      } else {
+        b = static_cast<int>(static_cast<double>(lh) * static_cast<double>(ures) * rD);
+        int64_t rm = static_cast<int64_t>(lh) * ures - static_cast<int64_t>(b) * D;
+        const bool lo = rm < 0, hi = rm >= D;
+        b += lo ? -1 : (hi ? 1 : 0);
+        rm += lo ? D : (hi ? -D : 0);
+        rem = static_cast<int>(rm);
+      }
+      const int left = lh - (kOneRow ? readlane(row_sum(b), 0) : wave_sum(b));
+      // the `left` hosts with the largest remainders (ties: earlier host)
+      int rk = 0;
+      for (int j = 0; j < nh; ++j) {
+        const int rj = readlane(rem, j);
+        rk += (rj > rem) || (rj == rem && j < lane);
+      }
+      qi = b + ((host && rk < left) ? 1 : 0);
+      ures -= qi;
+    }
+    if (host) qcol[r * ncol] = qi + (t_i == r ? qloc_i : 0);
+  }
+}
+
+// SolveReroute for expert e, run by one wave.  The hosts of e are its home
+// and every other rank with a positive quota (a replica's quota is at least
+// u_min), so the expert's row of U (u_r: its quota on rank `lane`), its load
+// column (lam_r), its first CSR column j0 and the number of CSR entries are
+// all the inputs.  Locality first: a host consumes its own tokens up to its
+// quota; the residual demands are then split over the residual quotas.
+__device__ void reroute_expert(const PlanArgs &a, int e, int j0, int total, int lam_r,
+                               int u_r, int64_t L, int32_t *s_t) {
+  const int lane = lane_id();
+  const int R = a.R, E = a.E;
+  const int64_t ncol = a.ncol;
+  const int h = e / a.nm;
+  const uint64_t rep = ballot(lane < R && lane != h && u_r > 0);
+  const int nh = 1 + __popcll(rep);
+  if (j0 < e || j0 + nh > total || total > ncol) {  // not a plan of this group
+    if (lane == 0) a.stats[6] = ULTRAEP_EDATA;
+    return;
+  }
+  const int loc_r = min(lam_r, u_r);  // 0 on ranks that do not host e
+  const int lamhat_r = lam_r - loc_r;
+  const int ures_r = u_r - loc_r;
+  // residual demand still to place when source r comes: D0 minus the
+  // demand of the sources before it
+  int incl = lamhat_r;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  const int D0 = readlane(incl, kWave - 1);
+  const int Dr = D0 - (incl - lamhat_r);
+  const bool exact = L < (int64_t(1) << 26);
+  int32_t *qrow = a.q + static_cast<int64_t>(lane) * ncol;
+  if (nh == 1) {
+    if (lane < R) qrow[j0] = lam_r;
+  } else if (nh == 2) {
+    const int t = __ffsll(static_cast<unsigned long long>(rep)) - 1;
+    const int u0 = readlane(ures_r, h);
+    const int q0 = exact ? split_two<true>(lamhat_r, Dr, u0, R)
+                         : split_two<false>(lamhat_r, Dr, u0, R);
+    if (lane < R) {
+      qrow[j0] = q0 + (lane == h ? loc_r : 0);
+      qrow[j0 + 1] = lamhat_r - q0 + (lane == t ? loc_r : 0);
+    }
+  } else if (exact && nh == 3) {
+    reroute_small<3>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
+  } else if (exact && nh == 4) {
+    reroute_small<4>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
+  } else {
+    if (lane == h) s_t[0] = h;
+    if ((rep >> lane) & 1) s_t[1 + popc_below(rep)] = lane;
+    __syncthreads();
+    const int t_i = lane < nh ? s_t[lane] : 0;
+    // every lane takes part in the shuffles: a lane reads only from lanes
+    // that execute the same shuffle
+    const int ures_t = __shfl(ures_r, t_i);
+    const int qloc_i = __shfl(loc_r, t_i);
+    const int ures_i = lane < nh ? ures_t : 0;
+    int32_t *qcol = a.q + j0 + lane;
+    if (exact && nh <= 16)
+      split_many<true, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (exact)
+      split_many<true, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (nh <= 16)
+      split_many<false, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else
+      split_many<false, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+  }
+  // CSR padding columns of Q
+  for (int j = total + e; j < ncol; j += E)
+    if (lane < R) qrow[j] = 0;
+}
+
 // ---------------------------------------------------------------- emit
 
+// kReroute: the same workgroup then runs SolveReroute for its expert from
+// the values it has just produced (ultraep_plan's single-launch ending).
+template <bool kReroute>
 __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
+  __shared__ int32_t s_t[kWave];
   __shared__ uint32_t s_et[kMaxRec];
   __shared__ int32_t s_d[kMaxRec];
   __shared__ int32_t s_ht[kMaxR];  // hosts of this expert: rank
@@ -607,6 +856,7 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   BisState fin = state_before(a, kRounds - 1);
   const uint64_t bw = lane < kBitWords ? a.ws.bits[(kRounds - 1) * kBitWords + lane] : 0;
   const int lam_e = a.ws.lam[e];
+  const int lam_r = kReroute && lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
   if (status != 0) {
     if (e == 0 && lane < 8) a.stats[lane] = lane == 6 ? ULTRAEP_EDATA : (lane == 7 ? L : 0);
     return;
@@ -711,254 +961,19 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
       a.stats[7] = L;
     }
   }
+  if (kReroute) reroute_expert(a, e, hp_e, E + nb, lam_r, u_r, L, s_t);
 }
 
-// ---------------------------------------------------------------- reroute
-
-// DPP wave_shr:1 - lane i receives lane i-1 (lane 0 keeps its value)
-__device__ __forceinline__ int wave_shr1(int v) {
-  return __builtin_amdgcn_update_dpp(v, v, 0x138, 0xF, 0xF, false);
-}
-
-// Two hosts (home first, one replica): with residual quotas (u0, u1) and
-// residual demand D = u0 + u1, a source with demand lh gives host 0
-// b0 = floor(lh * u0 / D) plus the one leftover unit when its remainder is
-// at least the other host's (ties go to the earlier host), i.e.
-// q0 = floor((lh * u0 + D / 2) / D).  The sources run in ascending order with
-// the state u0 carried from lane r to lane r + 1 by a DPP shift, so the chain
-// has no scalar round trip and no branch.  Lane r returns q0 of source r.
-//   kExact: lh * u0 + D / 2 < 2^52 (total load below 2^26), so the fp64
-//   numerator is exact and one correction of the reciprocal estimate
-//   gives the floor; otherwise the same in int64.
-template <bool kExact>
-__device__ int split_two(int lamhat, int Dr, int u0_init, int R) {
-  const bool act = lamhat > 0;
-  const double lhd = static_cast<double>(lamhat);
-  const double Dd = act ? static_cast<double>(Dr) : 1.0;
-  const double rD = 1.0 / Dd;
-  const double half = 0.5 * Dd;
-  int u0 = u0_init, qout = 0;
-  const int lane = lane_id();
-  for (int r = 0; r < R; ++r) {
-    int q;
-    if (kExact) {
-      const double N = __builtin_fma(lhd, static_cast<double>(u0), half);
-      const double t = __builtin_trunc(N * rD);
-      const double rr = __builtin_fma(-t, Dd, N);
-      q = static_cast<int>(t) + (rr >= Dd ? 1 : 0) - (rr < 0.0 ? 1 : 0);
-    } else {
-      const int64_t D = act ? Dr : 1;
-      const int64_t N = 2 * static_cast<int64_t>(lamhat) * u0 + D;
-      int64_t t = static_cast<int64_t>(static_cast<double>(N) * (0.5 * rD));
-      const int64_t rr = N - t * 2 * D;
-      t += (rr >= 2 * D ? 1 : 0) - (rr < 0 ? 1 : 0);
-      q = static_cast<int>(t);
-    }
-    qout = lane == r ? q : qout;
-    u0 = wave_shr1(u0 - q);
-  }
-  return qout;
-}
-
-// A few hosts (NH of them, home first): the same chain as split_two with
-// the residual quotas of hosts 0 .. NH-2 carried from lane r to lane r + 1;
-// the last host's quota is the rest of the residual demand.  Each source
-// computes the floor and remainder of lh * u_i / D for those hosts side by
-// side; for the last host they follow from the sum S of the others'
-// remainders, since all remainders add up to (leftover units) * D:
-// leftover = ceil(S / D) and its remainder is leftover * D - S.  The
-// leftover units go to the largest remainders (ties to the earlier host).
-// Needs lh * u below 2^52 (total load below 2^26).  Lane r returns source
-// r's share for each host in q[].
-template <int NH>
-__device__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH]) {
-  const bool act = lamhat > 0;
-  const double lhd = static_cast<double>(lamhat);
-  const int Di = act ? Dr : 1;
-  const double Dd = static_cast<double>(Di);
-  const double rD = 1.0 / Dd;
-  const int lane = lane_id();
-#pragma unroll
-  for (int i = 0; i < NH; ++i) q[i] = 0;
-  for (int r = 0; r < R; ++r) {
-    int b[NH], rem[NH];
-    int sb = 0, srem = 0;
-#pragma unroll
-    for (int i = 0; i < NH - 1; ++i) {
-      const double pr = lhd * static_cast<double>(u[i]);
-      const double t = __builtin_trunc(pr * rD);
-      const double rr = __builtin_fma(-t, Dd, pr);
-      const int lo = rr < 0.0 ? 1 : 0, hi = rr >= Dd ? 1 : 0;
-      b[i] = static_cast<int>(t) + hi - lo;
-      rem[i] = static_cast<int>(rr) + (lo ? Di : 0) - (hi ? Di : 0);
-      sb += b[i];
-      srem += rem[i];
-    }
-    // srem < (NH - 1) * D: leftover = ceil(srem / D), at most NH - 1
-    int left = 0;
-#pragma unroll
-    for (int k = 1; k < NH; ++k) left += srem > (k - 1) * Di ? 1 : 0;
-    rem[NH - 1] = left * Di - srem;
-    b[NH - 1] = lamhat - sb - left;
-    const bool me = lane == r;
-#pragma unroll
-    for (int i = 0; i < NH; ++i) {
-      int rk = 0;  // hosts ahead of i in (remainder descending, host ascending)
-#pragma unroll
-      for (int k = 0; k < NH; ++k)
-        if (k != i) rk += k < i ? (rem[k] >= rem[i] ? 1 : 0) : (rem[k] > rem[i] ? 1 : 0);
-      const int qi = b[i] + (rk < left ? 1 : 0);
-      q[i] = me ? qi : q[i];
-      if (i < NH - 1) u[i] = wave_shr1(u[i] - qi);
-    }
-  }
-}
-
-// Runs split_small for NH hosts: hosts' ranks t[] and residual quotas come
-// from the replica mask; writes rows of Q (lane = source rank).
-template <int NH>
-__device__ void reroute_small(int h, uint64_t rep, int lamhat_r, int Dr, int ures_r,
-                              int loc_r, int R, int32_t *qrow, int j0) {
-  const int lane = lane_id();
-  int t[NH], u[NH], q[NH];
-  t[0] = h;
-  uint64_t mrest = rep;
-#pragma unroll
-  for (int i = 1; i < NH; ++i) {
-    t[i] = __ffsll(static_cast<unsigned long long>(mrest)) - 1;
-    mrest &= mrest - 1;
-  }
-#pragma unroll
-  for (int i = 0; i < NH; ++i) u[i] = readlane(ures_r, t[i]);
-  split_small<NH>(lamhat_r, Dr, u, R, q);
-  if (lane < R) {
-#pragma unroll
-    for (int i = 0; i < NH; ++i) qrow[j0 + i] = q[i] + (lane == t[i] ? loc_r : 0);
-  }
-}
-
-// Any number of hosts: lane i is host i (home first, then replicas by
-// ascending rank) with residual quota ures; the sources run in ascending
-// order, each splitting its residual demand by largest remainder.  Writes
-// q of source r, host `lane` to qcol[r * ncol].
-template <bool kExact, bool kOneRow>
-__device__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int R,
-                           int64_t ncol, int32_t *qcol, int t_i, int qloc_i) {
-  const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
-  const bool host = lane < nh;
-  for (int r = 0; r < R; ++r) {
-    const int lh = readlane(lamhat_r, r);
-    int qi = 0;
-    if (lh > 0) {
-      const int D = readlane(Dr, r);
-      const double rD = readlane_d(rDr, r);
-      // floor(lh * ures / D) and its remainder, exact after one correction
-      int b, rem;
-      if (kExact) {  // lh * ures < 2^52
-        const double Dd = static_cast<double>(D);
-        const double pr = static_cast<double>(lh) * static_cast<double>(ures);
-        const double bq = __builtin_trunc(pr * rD);
-        const double rd = __builtin_fma(-bq, Dd, pr);
-        const int lo = rd < 0.0 ? 1 : 0, hi = rd >= Dd ? 1 : 0;
-        b = static_cast<int>(bq) + hi - lo;
-        rem = static_cast<int>(rd) + (lo ? D : 0) - (hi ? D : 0);
-      } else {
-        b = static_cast<int>(static_cast<double>(lh) * static_cast<double>(ures) * rD);
-        int64_t rm = static_cast<int64_t>(lh) * ures - static_cast<int64_t>(b) * D;
-        const bool lo = rm < 0, hi = rm >= D;
-        b += lo ? -1 : (hi ? 1 : 0);
-        rm += lo ? D : (hi ? -D : 0);
-        rem = static_cast<int>(rm);
-      }
-      const int left = lh - (kOneRow ? readlane(row_sum(b), 0) : wave_sum(b));
-      // the `left` hosts with the largest remainders (ties: earlier host)
-      int rk = 0;
-      for (int j = 0; j < nh; ++j) {
-        const int rj = readlane(rem, j);
-        rk += (rj > rem) || (rj == rem && j < lane);
-      }
-      qi = b + ((host && rk < left) ? 1 : 0);
-      ures -= qi;
-    }
-    if (host) qcol[r * ncol] = qi + (t_i == r ? qloc_i : 0);
-  }
-}
-
-// SolveReroute for expert blockIdx.x (one wave).  The hosts of e are its
-// home and every other rank with a positive quota (a replica's quota is at
-// least u_min), so U's row, the load column and the expert's first CSR
-// column are all the inputs, loaded together.  Locality first: a host
-// consumes its own tokens up to its quota; the residual demands are then
-// split over the residual quotas.
 __global__ void __launch_bounds__(kWave) k_plan_reroute(PlanArgs a) {
   __shared__ int32_t s_t[kWave];
   const int e = blockIdx.x, lane = threadIdx.x;
   const int R = a.R, E = a.E;
-  const int64_t ncol = a.ncol;
-  const int h = e / a.nm;
   const int64_t status = a.stats[6], L = a.stats[7];
   const int j0 = a.hp[e], total = a.hp[E];
   const int lam_r = lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
   const int u_r = lane < R ? a.U[static_cast<int64_t>(e) * R + lane] : 0;
   if (status != 0) return;
-  const uint64_t rep = ballot(lane < R && lane != h && u_r > 0);
-  const int nh = 1 + __popcll(rep);
-  if (j0 < e || j0 + nh > total || total > ncol) {  // not a plan of this group
-    if (lane == 0) a.stats[6] = ULTRAEP_EDATA;
-    return;
-  }
-  const int loc_r = min(lam_r, u_r);  // 0 on ranks that do not host e
-  const int lamhat_r = lam_r - loc_r;
-  const int ures_r = u_r - loc_r;
-  // residual demand still to place when source r comes: D0 minus the
-  // demand of the sources before it
-  int incl = lamhat_r;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(incl, o);
-    if (lane >= o) incl += t;
-  }
-  const int D0 = readlane(incl, kWave - 1);
-  const int Dr = D0 - (incl - lamhat_r);
-  const bool exact = L < (int64_t(1) << 26);
-  int32_t *qrow = a.q + static_cast<int64_t>(lane) * ncol;
-  if (nh == 1) {
-    if (lane < R) qrow[j0] = lam_r;
-  } else if (nh == 2) {
-    const int t = __ffsll(static_cast<unsigned long long>(rep)) - 1;
-    const int u0 = readlane(ures_r, h);
-    const int q0 = exact ? split_two<true>(lamhat_r, Dr, u0, R)
-                         : split_two<false>(lamhat_r, Dr, u0, R);
-    if (lane < R) {
-      qrow[j0] = q0 + (lane == h ? loc_r : 0);
-      qrow[j0 + 1] = lamhat_r - q0 + (lane == t ? loc_r : 0);
-    }
-  } else if (exact && nh == 3) {
-    reroute_small<3>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
-  } else if (exact && nh == 4) {
-    reroute_small<4>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
-  } else {
-    if (lane == h) s_t[0] = h;
-    if ((rep >> lane) & 1) s_t[1 + popc_below(rep)] = lane;
-    __syncthreads();
-    const int t_i = lane < nh ? s_t[lane] : 0;
-    // every lane takes part in the shuffles: a lane reads only from lanes
-    // that execute the same shuffle
-    const int ures_t = __shfl(ures_r, t_i);
-    const int qloc_i = __shfl(loc_r, t_i);
-    const int ures_i = lane < nh ? ures_t : 0;
-    int32_t *qcol = a.q + j0 + lane;
-    if (exact && nh <= 16)
-      split_many<true, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-    else if (exact)
-      split_many<true, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-    else if (nh <= 16)
-      split_many<false, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-    else
-      split_many<false, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-  }
-  // CSR padding columns of Q
-  for (int j = total + e; j < ncol; j += E)
-    if (lane < R) qrow[j] = 0;
+  reroute_expert(a, e, j0, total, lam_r, u_r, L, s_t);
 }
 
 static PlanArgs plan_args(const int32_t *load, const ultraep_group &g,
@@ -994,7 +1009,21 @@ hipError_t launch_plan_replicate(const int32_t *load, const ultraep_group &g,
     err = hipGetLastError();
   }
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_plan_emit, dim3(g.E), dim3(kWave), 0, stream, a);
+  hipLaunchKernelGGL(k_plan_emit<false>, dim3(g.E), dim3(kWave), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
+                       const ultraep_plan_buf &out, void *ws, hipStream_t stream) {
+  const PlanArgs a = plan_args(load, g, out, ws);
+  hipLaunchKernelGGL(k_plan_prep, dim3(1), dim3(kPrepThreads), 0, stream, a);
+  hipError_t err = hipGetLastError();
+  for (int round = 0; round < kRounds && err == hipSuccess; ++round) {
+    hipLaunchKernelGGL(k_plan_round, dim3(kNodes), dim3(kWave), 0, stream, a, round);
+    err = hipGetLastError();
+  }
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_plan_emit<true>, dim3(g.E), dim3(kWave), 0, stream, a);
   return hipGetLastError();
 }
 

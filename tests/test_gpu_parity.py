@@ -127,6 +127,31 @@ def test_fuzz_parity(seed):
 
 # ------------------------------------------------------------- error paths
 
+@pytest.mark.parametrize("seed,W", [(0, 1 << 19), (1, 1 << 19), (2, 3 << 21), (3, 1 << 12)])
+def test_pack_many_experts_and_tiles(seed, W):
+    """Several replicated local experts with unequal fan-out and enough tiles
+    to spread every expert over many workgroups: each (expert, tile) task
+    must be copied exactly once, to every destination."""
+    import types
+    R, E, NS, rank = 16, 64, 4, 3
+    g, og = gp.groups(R, E, NS, 1)
+    rng = np.random.default_rng(seed)
+    X = np.where(rng.random(R * NS) < 0.6,
+                 rank * 4 + rng.integers(0, 4, R * NS),
+                 rng.integers(-1, E, R * NS)).astype(np.int32)
+    w = rng.integers(0, 1 << 16, (E // R, W), dtype=np.uint16)
+    cap = R * NS
+    ostg, odoff, n_out, ost = oracle.pack(w, rank, og, types.SimpleNamespace(slot_expert=X), cap)
+    assert ost == 0 and n_out > 0
+    plan = uep.Plan(g, gp.DEV)
+    plan.slot_expert.copy_(torch.from_numpy(X))
+    stg, doff, st = gp.gpu_pack(w, rank, g, plan, cap)
+    assert st == 0
+    assert np.array_equal(doff, odoff)
+    assert np.array_equal(stg[:n_out], ostg[:n_out])
+    assert (stg[n_out:] == 0x3C3C).all()
+
+
 def test_count_flags_bad_ids():
     tk = np.array([[[0, 3], [16, -1]], [[-2, 1], [2, 2]]], np.int32)
     counts, st = gp.gpu_count(tk, 16)
