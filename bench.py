@@ -18,9 +18,10 @@ second stream next to reroute and dispatch, as the forward pipeline of
 Eq. (1) allows, measured slower on one GPU: the cross-queue dependencies of
 the graph cost more than the overlap gains, and the packing's workgroups
 crowd out the latency-bound kernels.)  The graph's outputs are checked
-against an eager step.  A second pass of K eager steps records HIP events
-around every launch on the launch stream; the dominant kernel's average
-duration gives the roofline figures.  The CPU oracle is timed
+against an eager step.  A second pass of K eager steps records a HIP event
+between consecutive launches on the launch stream; the dominant kernel's
+average duration gives the roofline figures, and count + plan is timed as
+one pair.  The CPU oracle is timed
 single-threaded on a bounded sample of the same workload.
 
 Prints one JSON line.
@@ -167,22 +168,27 @@ def main():
     t_graph = (time.perf_counter() - t_start) / args.steps
     del ref
 
-    # ---------------- eager pass with HIP events around every launch
+    # ---------------- eager pass with a HIP event between consecutive launches
+    # on the launch stream: call i lasts from event i to event i + 1
     stream = torch.cuda.current_stream()
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for _ in calls] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
-        for (name, f), (e0, e1) in zip(calls, evs[i]):
-            e0.record(stream)
+        evs[i][0].record(stream)
+        for j, (_, f) in enumerate(calls):
             f()
-            e1.record(stream)
+            evs[i][j + 1].record(stream)
     torch.cuda.synchronize()
     t_eager = (time.perf_counter() - t_start) / args.steps
-    per_call_us = {name: 1e3 * float(np.mean([evs[i][j][0].elapsed_time(evs[i][j][1])
-                                              for i in range(args.steps)]))
-                   for j, (name, _) in enumerate(calls)}
+
+    def span_us(j0, j1):
+        return 1e3 * float(np.mean([evs[i][j0].elapsed_time(evs[i][j1])
+                                    for i in range(args.steps)]))
+
+    per_call_us = {name: span_us(j, j + 1) for j, (name, _) in enumerate(calls)}
+    count_plan_us = span_us(0, 2)  # count and plan as one pair
     st = int(status.item())
     assert st == 0, f"device status {st}: {uep.ultraep_strerror(st)}"
     n_routed = int(boff[-1].item())
@@ -255,7 +261,7 @@ def main():
             "avg_launch_us": round(dus, 2),
         },
         "kernels_us": {n: round(v, 2) for n, v in per_call_us.items()},
-        "count_plan_us": round(per_call_us["count"] + per_call_us["plan"], 2),
+        "count_plan_us": round(count_plan_us, 2),
         "eager_us_per_step": round(t_eager * 1e6, 2),
         "dispatch_scatter_GBps": round(scatter_bytes / per_call_us["dispatch_scatter"] / 1e3, 1),
         "pack_GBps": round(pack_bytes / per_call_us["pack"] / 1e3, 1) if pack_bytes else None,

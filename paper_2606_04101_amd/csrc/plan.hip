@@ -682,13 +682,18 @@ __device__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH
     rem[NH - 1] = left * Di - srem;
     b[NH - 1] = lamhat - sb - left;
     const bool me = lane == r;
+    int extra[NH];
 #pragma unroll
     for (int i = 0; i < NH; ++i) {
       int rk = 0;  // hosts ahead of i in (remainder descending, host ascending)
 #pragma unroll
       for (int k = 0; k < NH; ++k)
         if (k != i) rk += k < i ? (rem[k] >= rem[i] ? 1 : 0) : (rem[k] > rem[i] ? 1 : 0);
-      const int qi = b[i] + (rk < left ? 1 : 0);
+      extra[i] = rk < left ? 1 : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      const int qi = b[i] + extra[i];
       q[i] = me ? qi : q[i];
       if (i < NH - 1) u[i] = wave_shr1(u[i] - qi);
     }
