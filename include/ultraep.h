@@ -109,7 +109,8 @@ int ultraep_plan_sizes(const ultraep_group *g, size_t counts_out[7]);
  * to expert e, for n_groups blocks of T * k ids stored back to back in topk
  * ([n_groups][T][k] int32).  Id -1 means "not routed" and is skipped; ids
  * outside [-1, E) are skipped and raise ULTRAEP_EDATA in *status.  One count
- * per routed slot (no per-token deduplication).  counts is fully written. */
+ * per routed slot (no per-token deduplication).  counts is fully written.
+ * 1 <= n_groups <= 65535, 1 <= k <= min(E, 64), E <= 1024, T * k < 2^31. */
 int ultraep_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
                   int32_t n_groups, int32_t *counts, int32_t *status,
                   hipStream_t stream);

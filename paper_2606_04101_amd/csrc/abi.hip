@@ -53,7 +53,8 @@ int ultraep_plan_sizes(const ultraep_group *g, size_t counts_out[7]) {
 int ultraep_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
                   int32_t n_groups, int32_t *counts, int32_t *status,
                   hipStream_t stream) {
-  if (E < 1 || E > 1024 || n_groups < 1 || !routing_ok(T, k, E) || !counts || !status)
+  if (E < 1 || E > 1024 || n_groups < 1 || n_groups > 65535 || !routing_ok(T, k, E) || !counts ||
+      !status)
     return ULTRAEP_EINVAL;
   if (T > 0 && !topk) return ULTRAEP_EINVAL;
   return rc(uep::launch_count(topk, T, k, E, n_groups, counts, status, stream));

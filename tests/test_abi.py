@@ -71,6 +71,7 @@ def test_invalid_arguments_return_einval_without_launch():
     assert L.ultraep_count(fake, 8, 0, 16, 1, fake, fake, None) == E      # k = 0
     assert L.ultraep_count(fake, 8, 17, 16, 1, fake, fake, None) == E     # k > E
     assert L.ultraep_count(fake, 8, 2, 16, 0, fake, fake, None) == E      # no groups
+    assert L.ultraep_count(fake, 8, 2, 16, 65536, fake, fake, None) == E  # too many groups
     assert L.ultraep_count(fake, 8, 2, 16, 1, fake, None, None) == E      # no status
     assert L.ultraep_plan(fake, ctypes.byref(g), ctypes.byref(pb), fake, 1 << 30, None) == E
     bad = uep.Group(4, 15, 2, 32)

@@ -159,6 +159,24 @@ def test_count_flags_bad_ids():
     assert counts[0].tolist()[:4] == [1, 0, 0, 1] and counts[1].tolist()[:3] == [0, 1, 2]
 
 
+@pytest.mark.parametrize("T,k,E,n_groups,bad", [(10001, 7, 96, 3, False), (8192, 8, 256, 2, False),
+                                                 (4097, 8, 64, 1, True), (40000, 1, 1024, 2, False)])
+def test_count_large_blocks(T, k, E, n_groups, bad):
+    """Blocks above 32768 ids take the multi-workgroup path (unaligned sizes,
+    masked slots, skewed ids, bad ids) and must equal the oracle."""
+    rng = np.random.default_rng(T + E)
+    hot = rng.integers(0, E, 4)
+    tk = np.where(rng.random((n_groups, T, k)) < 0.5, hot[rng.integers(0, 4, (n_groups, T, k))],
+                  rng.integers(-1, E, (n_groups, T, k))).astype(np.int32)
+    if bad:
+        tk[0, 17, 3] = E
+        tk[0, 4000, 0] = -5
+    counts, st = gp.gpu_count(tk, E)
+    ocounts, ost = oracle.count(tk, E, n_groups)
+    assert st == (uep.ULTRAEP_EDATA if bad else 0)
+    assert np.array_equal(counts, ocounts)
+
+
 def test_plan_flags_negative_load():
     g, og = gp.groups(4, 8, 1, 1)
     load = np.ones((4, 8), np.int32)
