@@ -14,9 +14,10 @@
 //                cumulative quota exceeds the ordinal and writes the row.
 // Scatter (bandwidth bound): one wave per token reads the token's row once
 //   into registers with 16-byte non-temporal loads and stores it to each of
-//   its k destination rows with 16-byte stores (plain stores measure faster
-//   than non-temporal ones for these 14 KiB rows); rows past the routed
-//   count are zero-filled.
+//   its k destination rows with 16-byte stores, each 1 KiB chunk to all k
+//   rows before the next (plain stores, chunk by chunk, measure faster than
+//   non-temporal stores or row by row for these 14 KiB rows); rows past the
+//   routed count are zero-filled.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -311,14 +312,15 @@ k_scatter(const v4u *__restrict__ x, int64_t T, int32_t k, int32_t nch,
         const int cc = c0 + u * kWave + lane;
         if (cc < nch) v[u] = __builtin_nontemporal_load(src + cc);
       }
-      for (int kk = 0; kk < k; ++kk) {
-        const int row = readlane(rows, kk);
-        if (row < 0 || row >= T * k) continue;
-        v4u *dst = send + static_cast<int64_t>(row) * nch;
+      // chunk by chunk, each to all k rows (measured faster than row by row)
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int cc = c0 + u * kWave + lane;
-          if (cc < nch) dst[cc] = v[u];
+      for (int u = 0; u < U; ++u) {
+        const int cc = c0 + u * kWave + lane;
+        if (cc < nch) {
+          for (int kk = 0; kk < k; ++kk) {
+            const int row = readlane(rows, kk);
+            if (row >= 0 && row < T * k) send[static_cast<int64_t>(row) * nch + cc] = v[u];
+          }
         }
       }
     }
