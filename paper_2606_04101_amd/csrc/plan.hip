@@ -8,16 +8,18 @@
 //   k_plan_prep   one workgroup: lambda_e, ell_r, the rank visiting order
 //                 (descending excess at any threshold is descending ell), each
 //                 rank's experts by descending load, tau_lo0 and tau_hi0.
-//   k_plan_round  x3 launches of 1023 one-wave workgroups.  Each workgroup
-//                 replays the walk of the earlier rounds from their stored
-//                 outcomes, then runs the probe of its node of the next depth-10
-//                 subtree of the bisection (one probe per wave on its own SIMD,
-//                 so the 1023 probes of a round run at single-probe latency).
-//                 Three depth-10 rounds cover any range below 2^30.  In a probe
-//                 lane t holds rank t's slack and slot count; the target of
-//                 largest slack (ties: lower rank) is one DPP wave max over a
-//                 packed (slack, rank) key; the accepted transfers are kept in
-//                 LDS and stored once at the end if the probe is feasible.
+//   k_plan_round  x2 launches of 1023 one-wave workgroups.  Each workgroup
+//                 replays the walk of the earlier round from its stored
+//                 outcome bits, then runs the probe of its node of the next
+//                 depth-10 subtree of the bisection (one probe per wave on its
+//                 own SIMD, so the 1023 probes of a round run at single-probe
+//                 latency).  Two rounds cover threshold ranges below 2^20,
+//                 which holds for every workload here; a longer bisection
+//                 ends with its remaining probes run one after another in
+//                 k_plan_emit.  A probe keeps the admissible targets as a
+//                 sorted list across the lanes and takes the targets an
+//                 expert drains whole with one ballot over the prefix sums of
+//                 their slacks; a feasible probe stores its transfers.
 //   k_plan_emit   one wave per expert: walks the last round to tau* and the
 //                 last feasible probe, and materialises that probe's record
 //                 into its expert's row of U, its CSR host list and its rank's
@@ -38,7 +40,7 @@ constexpr int kMaxR = 64;
 constexpr int kMaxRec = 256;               // R * n_slot: one transfer per slot at most
 constexpr int kDepth = 10;                 // bisection levels per round
 constexpr int kNodes = (1 << kDepth) - 1;  // probes per round
-constexpr int kRounds = 3;                 // 30 levels
+constexpr int kRounds = 2;                 // 20 levels, the rest in k_plan_emit
 constexpr int64_t kMaxLoad = int64_t(1) << 30;
 constexpr int kNotReached = INT32_MIN;
 constexpr int kPrepThreads = 1024;
@@ -261,7 +263,8 @@ __device__ __forceinline__ void load_experts(const PlanArgs &a, int r, int j0, i
 
 // One redundant slot per rank: every transfer uses up its target, so
 // transfer k goes to the k-th listed target and its record stays in lane k.
-__device__ int probe_one_slot(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
+template <int kSite>
+__device__ __forceinline__ int probe_one_slot(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
                               int as_r, int as_l, const int32_t *s_eorder,
                               const int32_t *s_elam, uint32_t *s_re, int32_t *s_rd) {
   const int R = a.R, nm = a.nm, u_min = a.u_min;
@@ -335,7 +338,8 @@ __device__ int probe_one_slot(const PlanArgs &a, int tau, int lane, int rk_r, in
 // slot after an expert's last (partial) transfer moves back to its place in
 // the list; the lanes it passes shift down by one (DPP) and P is patched.
 // The list entries are packed keys (slack << 6) | (63 - rank).
-__device__ int probe_multi(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
+template <int kSite>
+__device__ __forceinline__ int probe_multi(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
                            int as_r, int as_l, const int32_t *s_eorder,
                            const int32_t *s_elam, uint32_t *s_re, int32_t *s_rd) {
   const int R = a.R, nm = a.nm, NS = a.NS, u_min = a.u_min;
@@ -423,7 +427,8 @@ __device__ int probe_multi(const PlanArgs &a, int tau, int lane, int rk_r, int r
 // The same probe for slacks of 25 bits or more: lane t holds rank t's slack
 // and slot count, and the target is a wave max plus a ballot for the lowest
 // rank among ties.
-__device__ int probe_wide(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
+template <int kSite>
+__device__ __forceinline__ int probe_wide(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
                           int ell_lane, const int32_t *s_eorder, const int32_t *s_elam,
                           uint32_t *s_re, int32_t *s_rd) {
   int slk = lane < a.R ? max(tau - ell_lane, 0) : 0;
@@ -471,6 +476,20 @@ __device__ int probe_wide(const PlanArgs &a, int tau, int lane, int rk_r, int rk
   return n;
 }
 
+// One probe at tau with the variant the thresholds and slots allow.  kSite
+// gives every call site its own copy: shared by two kernels, the compiler
+// loses sight of the probes' scalar loop state.
+template <int kSite>
+__device__ __forceinline__ int run_probe(const PlanArgs &a, bool packed, int tau, int lane,
+                                         int rk_r, int rk_l, int as_r, int as_l, int ell_lane,
+                                         const int32_t *s_eorder, const int32_t *s_elam,
+                                         uint32_t *s_re, int32_t *s_rd) {
+  if (!packed) return probe_wide<kSite>(a, tau, lane, rk_r, rk_l, ell_lane, s_eorder, s_elam, s_re, s_rd);
+  if (a.NS == 1)
+    return probe_one_slot<kSite>(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
+  return probe_multi<kSite>(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
+}
+
 // Bisection state before round rd: the initial interval, or the state
 // after round rd - 1 that round rd's first workgroup published.
 struct BisState {
@@ -493,7 +512,7 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
 
 // The sequential bisection through round rd's depth-kDepth subtree, from
 // state st, over the round's outcome bits (word w in lane w).
-__device__ void walk_bits(uint64_t bw, int rd, BisState &st) {
+__device__ __forceinline__ void walk_bits(uint64_t bw, int rd, BisState &st) {
   int node = 0;
   for (int d = 0; d < kDepth && st.lo < st.hi; ++d) {
     const int64_t mid = (st.lo + st.hi) / 2;
@@ -571,12 +590,8 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
     const int rk_l = __shfl(ell_lane, rk_r);
     const int as_l = __shfl(ell_lane, as_r);
     __syncthreads();
-    if (!packed)
-      n = probe_wide(a, tau, lane, rk_r, rk_l, ell_lane, s_eorder, s_elam, s_re, s_rd);
-    else if (a.NS == 1)
-      n = probe_one_slot(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
-    else
-      n = probe_multi(a, tau, lane, rk_r, rk_l, as_r, as_l, s_eorder, s_elam, s_re, s_rd);
+    n = run_probe<0>(a, packed, tau, lane, rk_r, rk_l, as_r, as_l, ell_lane, s_eorder, s_elam,
+                  s_re, s_rd);
     if (n > 0) {
       __syncthreads();
       uint32_t *rec = a.ws.rec + (static_cast<int64_t>(round) * kNodes + b) * 2 * RS;
@@ -610,7 +625,7 @@ __device__ __forceinline__ int wave_shr1(int v) {
 //   numerator is exact and one correction of the reciprocal estimate
 //   gives the floor; otherwise the same in int64.
 template <bool kExact>
-__device__ int split_two(int lamhat, int Dr, int u0_init, int R) {
+__device__ __forceinline__ int split_two(int lamhat, int Dr, int u0_init, int R) {
   const bool act = lamhat > 0;
   const double lhd = static_cast<double>(lamhat);
   const double Dd = act ? static_cast<double>(Dr) : 1.0;
@@ -650,7 +665,7 @@ __device__ int split_two(int lamhat, int Dr, int u0_init, int R) {
 // Needs lh * u below 2^52 (total load below 2^26).  Lane r returns source
 // r's share for each host in q[].
 template <int NH>
-__device__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH]) {
+__device__ __forceinline__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH]) {
   const bool act = lamhat > 0;
   const double lhd = static_cast<double>(lamhat);
   const int Di = act ? Dr : 1;
@@ -703,7 +718,7 @@ __device__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH
 // Runs split_small for NH hosts: hosts' ranks t[] and residual quotas come
 // from the replica mask; writes rows of Q (lane = source rank).
 template <int NH>
-__device__ void reroute_small(int h, uint64_t rep, int lamhat_r, int Dr, int ures_r,
+__device__ __forceinline__ void reroute_small(int h, uint64_t rep, int lamhat_r, int Dr, int ures_r,
                               int loc_r, int R, int32_t *qrow, int j0) {
   const int lane = lane_id();
   int t[NH], u[NH], q[NH];
@@ -728,7 +743,7 @@ __device__ void reroute_small(int h, uint64_t rep, int lamhat_r, int Dr, int ure
 // order, each splitting its residual demand by largest remainder.  Writes
 // q of source r, host `lane` to qcol[r * ncol].
 template <bool kExact, bool kOneRow>
-__device__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int R,
+__device__ __forceinline__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int R,
                            int64_t ncol, int32_t *qcol, int t_i, int qloc_i) {
   const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
   const bool host = lane < nh;
@@ -776,7 +791,7 @@ __device__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int
 // column (lam_r), its first CSR column j0 and the number of CSR entries are
 // all the inputs.  Locality first: a host consumes its own tokens up to its
 // quota; the residual demands are then split over the residual quotas.
-__device__ void reroute_expert(const PlanArgs &a, int e, int j0, int total, int lam_r,
+__device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0, int total, int lam_r,
                                int u_r, int64_t L, int32_t *s_t) {
   const int lane = lane_id();
   const int R = a.R, E = a.E;
@@ -867,11 +882,52 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
     return;
   }
   walk_bits(bw, kRounds - 1, fin);
+  int nb = 0;  // transfers of the last feasible probe, read into s_et / s_d
+  if (fin.lo < fin.hi) {
+    // a bisection longer than the rounds: the remaining probes run here, one
+    // after another, the same ones in every workgroup
+    __shared__ int32_t s_eorder[kMaxE];
+    __shared__ int32_t s_elam[kMaxE];
+    __shared__ uint32_t s_re[kMaxRec];
+    __shared__ int32_t s_rd[kMaxRec];
+    for (int i = lane; i < E; i += kWave) {
+      s_eorder[i] = a.ws.eorder[i];
+      s_elam[i] = a.ws.elam[i];
+    }
+    const int rk_r = lane < R ? a.ws.rank_desc[lane] : 0;
+    const int as_r = lane < R ? a.ws.rank_asc[lane] : 0;
+    const int ell_lane = lane < R ? a.ws.ell[lane] : 0;
+    const int rk_l = __shfl(ell_lane, rk_r);
+    const int as_l = __shfl(ell_lane, as_r);
+    const bool packed = hi0 < (int64_t(1) << 25);
+    bool local = false;
+    __syncthreads();
+    while (fin.lo < fin.hi) {
+      const int64_t mid = (fin.lo + fin.hi) / 2;
+      ++fin.probes;
+      const int n = run_probe<1>(a, packed, static_cast<int>(mid), lane, rk_r, rk_l, as_r, as_l,
+                              ell_lane, s_eorder, s_elam, s_re, s_rd);
+      __syncthreads();
+      if (n >= 0) {
+        fin.hi = mid;
+        local = true;
+        nb = n;
+        for (int i = lane; i < n; i += kWave) {
+          s_et[i] = s_re[i];
+          s_d[i] = s_rd[i];
+        }
+      } else {
+        fin.lo = mid + 1;
+      }
+      __syncthreads();
+    }
+    if (local) fin.best = -2;  // records already in s_et / s_d
+  }
   const int64_t hi = fin.hi;
   const int n_probe = fin.probes;
   const int best = fin.best;
-  const int nb = best >= 0 ? a.ws.res[best] : 0;
   if (best >= 0) {
+    nb = a.ws.res[best];
     const uint32_t *rec = a.ws.rec + static_cast<int64_t>(best) * 2 * RS;
     for (int i = lane; i < nb; i += kWave) {
       s_et[i] = rec[2 * i];

@@ -48,7 +48,7 @@ def test_plan_sizes():
 def test_plan_ws_bytes():
     g = uep.Group(64, 256, 1, 1024)
     n = uep.ultraep_plan_ws_bytes(g)
-    assert n >= 3 * 1023 * (1 + 2 * 64) * 4
+    assert n >= 2 * 1023 * (1 + 2 * 64) * 4
     assert uep.ultraep_plan_ws_bytes(uep.Group(3, 8, 1, 1)) == 0
 
 

@@ -77,6 +77,34 @@ def test_dsv3_prefill_all_layers_plan():
 
 # ------------------------------------------------------------- dispatch + pack
 
+def _big_load(seed, R, E, base, hot, n_hot):
+    rng = np.random.default_rng(seed)
+    load = rng.integers(0, base, (R, E)).astype(np.int64)
+    for e in rng.choice(E, n_hot, replace=False):
+        load[:, e] += rng.integers(hot // 2, hot, R)
+    assert load.sum() <= (1 << 30)
+    return load.astype(np.int32)
+
+
+@pytest.mark.parametrize("seed,R,E,NS,base,hot,n_hot", [
+    (0, 8, 32, 2, 1 << 14, 1 << 20, 2),     # thresholds up to ~2^23: a long bisection
+    (1, 16, 64, 1, 1 << 12, 1 << 21, 3),    # one slot, long bisection, total below 2^26
+    (2, 8, 16, 3, 1 << 16, 1 << 23, 1),     # slack of 25 bits and more, total above 2^26
+    (3, 4, 8, 2, 1 << 20, 1 << 25, 1),      # total near 2^30
+    (4, 32, 128, 2, 1 << 10, 1 << 19, 4),   # several hosts per hot expert, large quotas
+])
+def test_plan_large_loads(seed, R, E, NS, base, hot, n_hot):
+    """Load matrices far larger than any synthetic workload: bisections of
+    more than 20 levels, slacks that need the wide probe, totals that need
+    the 64-bit split.  The plan must still equal the oracle's."""
+    load = _big_load(seed, R, E, base, hot, n_hot)
+    g, og = gp.groups(R, E, NS, 1024)
+    op = oracle.plan(load, og)
+    gp.assert_plan_equal(gp.gpu_plan(load, g), op)
+    gp.assert_plan_equal(gp.gpu_plan(load, g, split=True), op)
+    check_plan(load, og, op)
+
+
 def test_tiny_every_rank():
     c, g, og, tk = _workload(1, 0)
     load, _ = oracle.count(tk, c.E, c.R)
