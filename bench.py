@@ -21,7 +21,8 @@ crowd out the latency-bound kernels.)  The graph's outputs are checked
 against an eager step.  A second pass of K eager steps records a HIP event
 between consecutive launches on the launch stream; the dominant kernel's
 average duration gives the roofline figures, and count + plan is timed as
-one pair.  The CPU oracle is timed
+one pair (count_plan_eager_us).  count_plan_us is the same pair's device
+latency: 20 consecutive pairs in one graph, replayed, divided by 20.  The CPU oracle is timed
 single-threaded on a bounded sample of the same workload.
 
 Prints one JSON line.
@@ -193,6 +194,28 @@ def main():
     assert st == 0, f"device status {st}: {uep.ultraep_strerror(st)}"
     n_routed = int(boff[-1].item())
 
+    # ---------------- count + plan latency without host launch gaps: 20
+    # consecutive pairs captured in one graph (each pair waits for the one
+    # before it on the stream), one replay, divided by 20
+    n_pairs = 20
+    pair_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(pair_graph):
+        for _ in range(n_pairs):
+            calls[0][1]()
+            calls[1][1]()
+    pair_graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    pair_us = []
+    for _ in range(5):
+        e0.record()
+        pair_graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        pair_us.append(1e3 * e0.elapsed_time(e1) / n_pairs)
+    count_plan_graph_us = float(np.median(pair_us))
+    del pair_graph
+
     # ---------------- a plain copy of known size (achievable bandwidth and
     # the reference kernel for scaling the HBM byte counters)
     a = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
@@ -261,7 +284,8 @@ def main():
             "avg_launch_us": round(dus, 2),
         },
         "kernels_us": {n: round(v, 2) for n, v in per_call_us.items()},
-        "count_plan_us": round(count_plan_us, 2),
+        "count_plan_us": round(count_plan_graph_us, 2),
+        "count_plan_eager_us": round(count_plan_us, 2),
         "eager_us_per_step": round(t_eager * 1e6, 2),
         "dispatch_scatter_GBps": round(scatter_bytes / per_call_us["dispatch_scatter"] / 1e3, 1),
         "pack_GBps": round(pack_bytes / per_call_us["pack"] / 1e3, 1) if pack_bytes else None,

@@ -654,6 +654,11 @@ __device__ __forceinline__ int split_two(int lamhat, int Dr, int u0_init, int R)
   return qout;
 }
 
+// 1 if a < b, for |a - b| < 2^31: the sign of the difference, no compare
+__device__ __forceinline__ int lt01(int a, int b) {
+  return static_cast<int>(static_cast<uint32_t>(a - b) >> 31);
+}
+
 // A few hosts (NH of them, home first): the same chain as split_two with
 // the residual quotas of hosts 0 .. NH-2 carried from lane r to lane r + 1;
 // the last host's quota is the rest of the residual demand.  Each source
@@ -684,31 +689,26 @@ __device__ __forceinline__ void split_small(int lamhat, int Dr, int (&u)[NH], in
       const int bi = static_cast<int>(lhd * static_cast<double>(u[i]) * rD);
       const int ri = static_cast<int>(static_cast<uint32_t>(lamhat) * static_cast<uint32_t>(u[i]) -
                                       static_cast<uint32_t>(bi) * static_cast<uint32_t>(Di));
-      const int lo = ri < 0 ? 1 : 0, hi = ri >= Di ? 1 : 0;
+      const int lo = lt01(ri, 0), hi = 1 - lt01(ri, Di);
       b[i] = bi + hi - lo;
-      rem[i] = ri + (lo ? Di : 0) - (hi ? Di : 0);
+      rem[i] = ri + (lo - hi) * Di;
       sb += b[i];
       srem += rem[i];
     }
     // srem < (NH - 1) * D: leftover = ceil(srem / D), at most NH - 1
     int left = 0;
 #pragma unroll
-    for (int k = 1; k < NH; ++k) left += srem > (k - 1) * Di ? 1 : 0;
+    for (int k = 1; k < NH; ++k) left += lt01((k - 1) * Di, srem);
     rem[NH - 1] = left * Di - srem;
     b[NH - 1] = lamhat - sb - left;
     const bool me = lane == r;
-    int extra[NH];
 #pragma unroll
     for (int i = 0; i < NH; ++i) {
       int rk = 0;  // hosts ahead of i in (remainder descending, host ascending)
 #pragma unroll
       for (int k = 0; k < NH; ++k)
-        if (k != i) rk += k < i ? (rem[k] >= rem[i] ? 1 : 0) : (rem[k] > rem[i] ? 1 : 0);
-      extra[i] = rk < left ? 1 : 0;
-    }
-#pragma unroll
-    for (int i = 0; i < NH; ++i) {
-      const int qi = b[i] + extra[i];
+        if (k != i) rk += k < i ? 1 - lt01(rem[k], rem[i]) : lt01(rem[i], rem[k]);
+      const int qi = b[i] + lt01(rk, left);
       q[i] = me ? qi : q[i];
       if (i < NH - 1) u[i] = wave_shr1(u[i] - qi);
     }
