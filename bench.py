@@ -3,9 +3,10 @@
 
 One step = one layer-microbatch of the hot path on the measured rank:
   count      (that rank's top-k ids -> its row of the load matrix)
-  plan       (SolveReplication then SolveReroute over the whole EP group)
+  replicate  (SolveReplication over the whole EP group)
+  reroute + pack  (SolveReroute, and the replicated main-expert blobs into
+             per-destination staging, in one launch: the overlap of Eq. (1))
   dispatch   layout + row scatter (bf16 rows into per-replica send blocks)
-  pack       (replicated main-expert blobs into per-destination staging)
 on synthetic DeepSeek-V3-shaped training routing (E=256, top-8 with
 8-group / top-4-group restriction, EP=64, one redundant slot per rank,
 4096 tokens per rank, H=7168, F=2048).  The other 63 ranks' load rows are
@@ -14,10 +15,8 @@ measured rank is the one with the most outbound replica bytes.
 
 Timed region: K replays of the step captured in one HIP graph on one
 stream, bracketed by device synchronisation.  (Running the packing on a
-second stream next to reroute and dispatch, as the forward pipeline of
-Eq. (1) allows, measured slower on one GPU: the cross-queue dependencies of
-the graph cost more than the overlap gains, and the packing's workgroups
-crowd out the latency-bound kernels.)  The graph's outputs are checked
+second stream instead measured slower on one GPU: the cross-queue
+dependencies of the graph cost more than the overlap gains.)  The graph's outputs are checked
 against an eager step.  A second pass of K eager steps records a HIP event
 between consecutive launches on the launch stream; the dominant kernel's
 average duration gives the roofline figures, and count + plan is timed as
@@ -125,13 +124,13 @@ def main():
 
     calls = [
         ("count", lambda: uep.ultraep_count(topk_r, T, k, c.E, 1, load_r, status)),
-        ("plan", lambda: uep.ultraep_plan(load, g, plan)),
+        ("plan_replicate", lambda: uep.ultraep_plan_replicate(load, g, plan)),
+        ("reroute_and_pack", lambda: uep.ultraep_reroute_and_pack(
+            load, g, plan, w, W, rank, staging, cap, doff, status)),
         ("dispatch_layout", lambda: uep.ultraep_dispatch_layout(
             topk_r, T, k, rank, g, plan, ros, boff, ws, status)),
         ("dispatch_scatter", lambda: uep.ultraep_dispatch_scatter(
             x, T, k, H, ros, boff[-1:], send)),
-        ("pack", lambda: uep.ultraep_pack_replicas(
-            w, W, rank, g, plan, staging, cap, doff, status)),
     ]
 
     def step():
@@ -189,7 +188,27 @@ def main():
                                     for i in range(args.steps)]))
 
     per_call_us = {name: span_us(j, j + 1) for j, (name, _) in enumerate(calls)}
-    count_plan_us = span_us(0, 2)  # count and plan as one pair
+
+    # ---------------- the pieces measured on their own, event-timed: the
+    # packing kernel alone (its bandwidth), and count + ultraep_plan (the
+    # reroute fused into the planner's last kernel) as one pair
+    def eager_us(fns, reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        torch.cuda.synchronize()
+        e[0].record(stream)
+        for i in range(reps):
+            for f in fns:
+                f()
+            e[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return 1e3 * float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(reps)]))
+
+    count_fn = calls[0][1]
+    plan_fn = lambda: uep.ultraep_plan(load, g, plan)
+    pack_fn = lambda: uep.ultraep_pack_replicas(w, W, rank, g, plan, staging, cap, doff, status)
+    per_call_us["pack"] = eager_us([pack_fn], args.steps)
+    per_call_us["plan"] = eager_us([plan_fn], args.steps)
+    count_plan_us = eager_us([count_fn, plan_fn], args.steps)
     st = int(status.item())
     assert st == 0, f"device status {st}: {uep.ultraep_strerror(st)}"
     n_routed = int(boff[-1].item())
@@ -201,8 +220,8 @@ def main():
     pair_graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(pair_graph):
         for _ in range(n_pairs):
-            calls[0][1]()
-            calls[1][1]()
+            count_fn()
+            plan_fn()
     pair_graph.replay()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -239,7 +258,7 @@ def main():
     kern = {
         "dispatch_scatter": (scatter_bytes, per_call_us["dispatch_scatter"],
                              ["dispatch.hip", "common.hpp"]),
-        "pack": (pack_bytes, per_call_us["pack"], ["pack.hip", "common.hpp"]),
+        "pack": (pack_bytes, per_call_us["pack"], ["pack.hip", "pack_core.hpp", "common.hpp"]),
     }
     dom = max(kern, key=lambda n: kern[n][1])
     dbytes, dus, dsrc = kern[dom]
@@ -270,7 +289,8 @@ def main():
             "routed_rows": n_routed,
             "replicas_shipped": int(n_out_r[rank]),
             "expert_blob_bytes": W_bytes,
-            "timed": "HIP graph replay of count, plan, dispatch layout, scatter, pack",
+            "timed": ("HIP graph replay of count, replicate, reroute + pack, "
+                      "dispatch layout, scatter"),
         },
         "roofline": {
             "kernel": dom,

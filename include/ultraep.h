@@ -211,6 +211,16 @@ int ultraep_pack_replicas(const uint16_t *w_main, int64_t W, int32_t rank,
                           uint16_t *staging, int64_t cap, int64_t *dest_off,
                           int32_t *status, hipStream_t stream);
 
+/* SolveReroute of ultraep_plan_reroute and the packing of
+ * ultraep_pack_replicas in one launch, overlapped as the forward pipeline of
+ * Sec. 4.2 overlaps the reroute with the weight distribution (Eq. (1)): the
+ * same results as the two calls.  Needs the buffers ultraep_plan_replicate
+ * wrote; arguments and errors as for the two calls. */
+int ultraep_reroute_and_pack(const int32_t *load, const ultraep_group *g,
+                             const ultraep_plan_buf *plan, const uint16_t *w_main, int64_t W,
+                             int32_t rank, uint16_t *staging, int64_t cap, int64_t *dest_off,
+                             int32_t *status, hipStream_t stream);
+
 /* Host only.  Static description of a status code. */
 const char *ultraep_strerror(int code);
 

@@ -91,12 +91,15 @@ def lib():
         L.ultraep_dispatch_scatter.argtypes = [_P, i64, i32, i32, _P, _P, _P, _P]
         L.ultraep_pack_replicas.argtypes = [_P, i64, i32, gp, pp, _P, i64, _P,
                                             _P, _P]
+        L.ultraep_reroute_and_pack.argtypes = [_P, gp, pp, _P, i64, i32, _P, i64, _P,
+                                               _P, _P]
         L.ultraep_strerror.argtypes = [ctypes.c_int]
         L.ultraep_strerror.restype = ctypes.c_char_p
         for f in ("ultraep_plan_sizes", "ultraep_count", "ultraep_plan",
                   "ultraep_plan_replicate", "ultraep_plan_reroute",
                   "ultraep_dispatch", "ultraep_dispatch_layout",
-                  "ultraep_dispatch_scatter", "ultraep_pack_replicas"):
+                  "ultraep_dispatch_scatter", "ultraep_pack_replicas",
+                  "ultraep_reroute_and_pack"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -220,6 +223,14 @@ def ultraep_pack_replicas(w_main, W, rank, g: Group, plan: Plan, staging, cap,
         _ptr(w_main), W, rank, ctypes.byref(g), ctypes.byref(plan.c),
         _ptr(staging), cap, _ptr(dest_off), _ptr(status), _stream(stream)),
         "ultraep_pack_replicas")
+
+
+def ultraep_reroute_and_pack(load, g: Group, plan: Plan, w_main, W, rank, staging,
+                             cap, dest_off, status, stream=None):
+    return _check(lib().ultraep_reroute_and_pack(
+        _ptr(load), ctypes.byref(g), ctypes.byref(plan.c), _ptr(w_main), W, rank,
+        _ptr(staging), cap, _ptr(dest_off), _ptr(status), _stream(stream)),
+        "ultraep_reroute_and_pack")
 
 
 def build():

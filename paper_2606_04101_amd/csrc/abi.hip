@@ -142,6 +142,17 @@ int ultraep_pack_replicas(const uint16_t *w_main, int64_t W, int32_t rank,
   return rc(uep::launch_pack(w_main, W, rank, *g, *plan, staging, cap, dest_off, status, stream));
 }
 
+int ultraep_reroute_and_pack(const int32_t *load, const ultraep_group *g,
+                             const ultraep_plan_buf *plan, const uint16_t *w_main, int64_t W,
+                             int32_t rank, uint16_t *staging, int64_t cap, int64_t *dest_off,
+                             int32_t *status, hipStream_t stream) {
+  if (!load || !group_ok(g) || !plan_ok(g, plan) || rank < 0 || rank >= g->R) return ULTRAEP_EINVAL;
+  if (W < 8 || W % 8 != 0 || cap < 0 || !dest_off || !status || !w_main) return ULTRAEP_EINVAL;
+  if (!aligned16(w_main) || (cap > 0 && (!staging || !aligned16(staging)))) return ULTRAEP_EINVAL;
+  return rc(uep::launch_reroute_pack(load, *g, *plan, w_main, W, rank, staging, cap, dest_off,
+                                     status, stream));
+}
+
 const char *ultraep_strerror(int code) {
   switch (code) {
     case ULTRAEP_OK: return "ok";

@@ -18,6 +18,11 @@ hipError_t launch_plan_replicate(const int32_t *load, const ultraep_group &g,
                                  const ultraep_plan_buf &out, void *ws, hipStream_t stream);
 hipError_t launch_plan_reroute(const int32_t *load, const ultraep_group &g,
                                const ultraep_plan_buf &out, hipStream_t stream);
+// SolveReroute and the local weight packing in one launch
+hipError_t launch_reroute_pack(const int32_t *load, const ultraep_group &g,
+                               const ultraep_plan_buf &out, const uint16_t *w_main, int64_t W,
+                               int32_t rank, uint16_t *staging, int64_t cap, int64_t *dest_off,
+                               int32_t *status, hipStream_t stream);
 // both halves, the reroute fused into the last kernel of the replication
 hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
                        const ultraep_plan_buf &out, void *ws, hipStream_t stream);

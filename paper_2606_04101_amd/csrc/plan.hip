@@ -32,6 +32,7 @@
 //                 does (Eq. 1).
 #include "common.hpp"
 #include "kernels.hpp"
+#include "pack_core.hpp"
 
 namespace uep {
 
@@ -1037,6 +1038,30 @@ __global__ void __launch_bounds__(kWave) k_plan_reroute(PlanArgs a) {
   reroute_expert(a, e, j0, total, lam_r, u_r, L, s_t);
 }
 
+// SolveReroute and the local weight packing in one launch, as the forward
+// pipeline overlaps them (Eq. 1): workgroup e < E runs expert e's split on
+// its first wave, the others pack tiles.  Packing needs only the replica
+// placement, which SolveReplication has already written.  The reroute
+// workgroups come first so they are placed before the packing fills the
+// chip.
+__global__ void __launch_bounds__(kPkThreads) k_reroute_pack(PlanArgs a, PkArgs p) {
+  __shared__ int32_t s_t[kWave];
+  const int b = blockIdx.x;
+  if (b < a.E) {
+    if (threadIdx.x >= kWave) return;
+    const int e = b, lane = threadIdx.x;
+    const int R = a.R, E = a.E;
+    const int64_t status = a.stats[6], L = a.stats[7];
+    const int j0 = a.hp[e], total = a.hp[E];
+    const int lam_r = lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
+    const int u_r = lane < R ? a.U[static_cast<int64_t>(e) * R + lane] : 0;
+    if (status != 0) return;
+    reroute_expert(a, e, j0, total, lam_r, u_r, L, s_t);
+    return;
+  }
+  pack_block(p, b - a.E, static_cast<int64_t>(gridDim.x) - a.E, b == a.E);
+}
+
 static PlanArgs plan_args(const int32_t *load, const ultraep_group &g,
                           const ultraep_plan_buf &out, void *ws) {
   PlanArgs a{};
@@ -1085,6 +1110,16 @@ hipError_t launch_plan(const int32_t *load, const ultraep_group &g,
   }
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(k_plan_emit<true>, dim3(g.E), dim3(kWave), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_reroute_pack(const int32_t *load, const ultraep_group &g,
+                               const ultraep_plan_buf &out, const uint16_t *w_main, int64_t W,
+                               int32_t rank, uint16_t *staging, int64_t cap, int64_t *dest_off,
+                               int32_t *status, hipStream_t stream) {
+  const PlanArgs a = plan_args(load, g, out, nullptr);
+  const PkArgs p = pack_args(w_main, W, rank, g, out, staging, cap, dest_off, status);
+  hipLaunchKernelGGL(k_reroute_pack, dim3(g.E + kPkGrid), dim3(kPkThreads), 0, stream, a, p);
   return hipGetLastError();
 }
 

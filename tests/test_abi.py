@@ -21,7 +21,7 @@ def declared_symbols():
 def test_header_declares_the_entry_points():
     names = declared_symbols()
     for n in ("ultraep_count", "ultraep_plan", "ultraep_dispatch",
-              "ultraep_plan_replicate", "ultraep_plan_reroute",
+              "ultraep_plan_replicate", "ultraep_plan_reroute", "ultraep_reroute_and_pack",
               "ultraep_dispatch_layout", "ultraep_dispatch_scatter",
               "ultraep_pack_replicas", "ultraep_plan_sizes",
               "ultraep_dispatch_ws_bytes", "ultraep_strerror"):
@@ -94,6 +94,12 @@ def test_invalid_arguments_return_einval_without_launch():
     assert L.ultraep_dispatch(fake, fake, 8, 2, 16, 0, ctypes.byref(g),  # small ws
                               ctypes.byref(full), fake, fake, fake, fake, 16,
                               fake, None) == E
+    for args in [(None, g, full, fake, 16, 0), (fake, bad, full, fake, 16, 0),   # load, group
+                 (fake, g, full, fake, 12, 0), (fake, g, full, fake, 16, 4),     # W % 8, rank
+                 (fake, g, pb, fake, 16, 0)]:                                     # plan
+        ld, gg, pl, w, W, rank = args
+        assert L.ultraep_reroute_and_pack(ld, ctypes.byref(gg), ctypes.byref(pl), w, W, rank,
+                                          fake, 4, fake, fake, None) == E
     odd = ctypes.c_void_p(4096 + 4)
     assert L.ultraep_dispatch_scatter(odd, 8, 2, 16, fake, fake, fake, None) == E
     assert L.ultraep_pack_replicas(fake, 12, 0, ctypes.byref(g), ctypes.byref(full),

@@ -180,6 +180,38 @@ def test_pack_many_experts_and_tiles(seed, W):
     assert (stg[n_out:] == 0x3C3C).all()
 
 
+@pytest.mark.parametrize("cid,m,rank_pick", [(1, 0, "max"), (2, 0, "max"), (3, 5, "max"),
+                                              (4, 0, "max"), (4, 0, "min"), (5, 11, "max")])
+def test_reroute_and_pack(cid, m, rank_pick):
+    """SolveReroute and the packing in one launch equal the oracle's plan and
+    staging."""
+    c, g, og, tk = _workload(cid, m)
+    load, _ = oracle.count(tk, c.E, c.R)
+    op = oracle.plan(load, og)
+    outb = [int(((op.slot_expert >= 0) & (op.slot_expert // c.n_main == r)).sum()) for r in range(c.R)]
+    rank = int(np.argmax(outb)) if rank_pick == "max" else int(np.argmin(outb))
+    W = 8 * 4096 if cid > 1 else c.W
+    w = gen.weights(c, rank, W=W)
+    cap = c.R * c.n_slot
+    ostg, odoff, n_out, ost = oracle.pack(w, rank, og, op, cap)
+    plan = uep.Plan(g, gp.DEV)
+    for f in uep.PLAN_FIELDS:
+        getattr(plan, f).fill_(-12345)
+    ld = gp.dev_i32(load)
+    uep.ultraep_plan_replicate(ld, g, plan)
+    st = gp.zero_status()
+    stg = torch.full((cap, W), 0x3C3C, dtype=torch.int16, device=gp.DEV)
+    doff = torch.full((c.R + 1,), -9, dtype=torch.int64, device=gp.DEV)
+    uep.ultraep_reroute_and_pack(ld, g, plan, gp.dev_u16(w), W, rank, stg, cap, doff, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    gp.assert_plan_equal(plan, op)
+    assert np.array_equal(doff.cpu().numpy(), odoff)
+    s = gp.host_u16(stg)
+    assert np.array_equal(s[:n_out], ostg[:n_out])
+    assert (s[n_out:] == 0x3C3C).all()
+
+
 def test_count_flags_bad_ids():
     tk = np.array([[[0, 3], [16, -1]], [[-2, 1], [2, 2]]], np.int32)
     counts, st = gp.gpu_count(tk, 16)
