@@ -13,8 +13,11 @@ on synthetic DeepSeek-V3-shaped training routing (E=256, top-8 with
 resident inputs (the all-gather that delivers them is not on one GPU).  The
 measured rank is the one with the most outbound replica bytes.
 
-Timed region: K replays of the step captured in one HIP graph on one
-stream, bracketed by device synchronisation.  (Running the packing on a
+Timed region: K steps as HIP graph replays on one stream, bracketed by
+device synchronisation; a graph holds 10 consecutive steps (when 10 divides
+K), so a step does not pay a whole graph launch alone, as it would not inside
+a larger training or serving graph.  one_step_graph_us reports the same
+steps launched one graph per step.  (Running the packing on a
 second stream instead measured slower on one GPU: the cross-queue
 dependencies of the graph cost more than the overlap gains.)  The graph's outputs are checked
 against an eager step.  A second pass of K eager steps records a HIP event
@@ -144,29 +147,50 @@ def main():
     torch.cuda.synchronize()
     ref = [t.clone() for t in outputs]
 
-    # ---------------- timed region: K graph replays of the whole step
-    graph = torch.cuda.CUDAGraph()
+    # ---------------- timed region: K steps as graph replays.  A graph holds
+    # G consecutive steps (G = 10 when it divides K): a step launched inside a
+    # larger graph, as a training or serving step would launch its layers,
+    # does not pay the fixed cost of a graph launch (about 8 µs here) alone.
+    G = 10 if args.steps % 10 == 0 else 1
+
+    def make_graph(n_steps):
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for _ in range(n_steps):
+                step()
+        return gr
+
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
         step()
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
-    with torch.cuda.graph(graph):
-        step()
+    graph = make_graph(G)
     for t in outputs:
         t.fill_(-1)
-    for _ in range(max(1, args.warmup)):
+    for _ in range(max(1, args.warmup // G)):
         graph.replay()
     torch.cuda.synchronize()
     for a, b in zip(outputs, ref):
         assert torch.equal(a, b), "graph replay differs from the eager step"
     t_start = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(args.steps // G):
         graph.replay()
     torch.cuda.synchronize()
     t_graph = (time.perf_counter() - t_start) / args.steps
-    del ref
+    del ref, graph
+    # the same steps with one step per graph launch, for reference
+    graph1 = make_graph(1)
+    for _ in range(max(1, args.warmup)):
+        graph1.replay()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        graph1.replay()
+    torch.cuda.synchronize()
+    t_graph1 = (time.perf_counter() - t_start) / args.steps
+    del graph1
 
     # ---------------- eager pass with a HIP event between consecutive launches
     # on the launch stream: call i lasts from event i to event i + 1
@@ -289,8 +313,9 @@ def main():
             "routed_rows": n_routed,
             "replicas_shipped": int(n_out_r[rank]),
             "expert_blob_bytes": W_bytes,
-            "timed": ("HIP graph replay of count, replicate, reroute + pack, "
+            "timed": ("HIP graph replays of count, replicate, reroute + pack, "
                       "dispatch layout, scatter"),
+            "steps_per_graph": G,
         },
         "roofline": {
             "kernel": dom,
@@ -306,6 +331,7 @@ def main():
         "kernels_us": {n: round(v, 2) for n, v in per_call_us.items()},
         "count_plan_us": round(count_plan_graph_us, 2),
         "count_plan_eager_us": round(count_plan_us, 2),
+        "one_step_graph_us": round(t_graph1 * 1e6, 2),
         "eager_us_per_step": round(t_eager * 1e6, 2),
         "dispatch_scatter_GBps": round(scatter_bytes / per_call_us["dispatch_scatter"] / 1e3, 1),
         "pack_GBps": round(pack_bytes / per_call_us["pack"] / 1e3, 1) if pack_bytes else None,
