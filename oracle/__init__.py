@@ -83,8 +83,11 @@ def _load(path):
                                _P, _P, _P, _P, _P]
     L.orc_pack.argtypes = [_P, i64, i32, gp, _P, _P, i64, _P, _P]
     L.orc_metrics.argtypes = [_P, gp, _P, _P, _P, _P, _P]
+    L.orc_relay.argtypes = [gp, _P, _P, _P, _P, i32, _P, _P, _P]
+    L.orc_pack_relay.argtypes = [_P, _P, i64, i32, gp, _P, _P, _P, i64, _P, _P]
     for f in ("orc_count", "orc_probe", "orc_plan", "orc_bisect_trace",
-              "orc_apportion", "orc_dispatch", "orc_pack", "orc_metrics"):
+              "orc_apportion", "orc_dispatch", "orc_pack", "orc_metrics",
+              "orc_relay", "orc_pack_relay"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -223,6 +226,49 @@ def pack(w_main, rank, g: Group, p: Plan, cap):
     st = lib().orc_pack(_p(w_main), W, rank, ctypes.byref(gc), _p(X),
                         _p(staging) if staging.size else None, cap, _p(doff),
                         _p(n_out))
+    return staging, doff, int(n_out[0]), st
+
+
+@dataclass
+class Relay:
+    slot_src: np.ndarray   # [R, n_slot] sender rank of each redundant slot, -1 empty
+    send_vol: np.ndarray   # [R] blobs sent per rank
+    stats: np.ndarray      # [4] relay experts, relays, max volume before / after
+    status: int
+
+
+def relay(g: Group, p, threshold=4) -> Relay:
+    """Relay trees (Sec. 6.2) of a plan; p needs slot_expert, host_ptr,
+    host_rank and host_pslot."""
+    ns = max(g.n_slot, 0)
+    X = _c(p.slot_expert, np.int32).reshape(-1)
+    src = np.full(max(g.R * ns, 1), -7, np.int32)
+    vol = np.full(g.R, -7, np.int32)
+    stats = np.zeros(4, np.int64)
+    gc = g.c()
+    st = lib().orc_relay(ctypes.byref(gc), _p(X) if X.size else _p(np.zeros(1, np.int32)),
+                         _p(_c(p.host_ptr, np.int32)), _p(_c(p.host_rank, np.int32)),
+                         _p(_c(p.host_pslot, np.int32)), int(threshold), _p(src),
+                         _p(vol), _p(stats))
+    return Relay(src[: g.R * ns].reshape(g.R, ns), vol, stats, st)
+
+
+def pack_relay(w_main, relay_src, rank, g: Group, slot_expert, slot_src, cap):
+    """-> staging [cap, W] uint16 (first n_out entries), dest_off [R+1], n_out, st"""
+    w_main = _c(w_main, np.uint16)
+    W = w_main.shape[1]
+    rs = None if relay_src is None else _c(relay_src, np.uint16)
+    staging = np.zeros((max(cap, 0), W), np.uint16)
+    doff = np.zeros(g.R + 1, np.int64)
+    n_out = np.zeros(1, np.int64)
+    gc = g.c()
+    X = _c(slot_expert, np.int32).reshape(-1)
+    S = _c(slot_src, np.int32).reshape(-1)
+    z = np.zeros(1, np.int32)
+    st = lib().orc_pack_relay(_p(w_main), _p(rs), W, rank, ctypes.byref(gc),
+                              _p(X) if X.size else _p(z), _p(S) if S.size else _p(z),
+                              _p(staging) if staging.size else None, cap, _p(doff),
+                              _p(n_out))
     return staging, doff, int(n_out[0]), st
 
 

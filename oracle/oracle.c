@@ -546,6 +546,181 @@ int orc_pack(const uint16_t *w_main, int64_t W, int32_t rank,
 }
 
 /* ------------------------------------------------------------------ */
+/* Relay trees for hot-expert fan-out (Sec. 6.2, "Load-Aware Relay    */
+/* Scheduling")                                                       */
+/* ------------------------------------------------------------------ */
+
+/* Integer nearest to sqrt(f) for f >= 0.  For an integer f, sqrt(f) is never
+ * a half-integer, so the rounding has no ties: with n = floor(sqrt(f)),
+ * round up iff f > n^2 + n (that is, f >= (n + 1/2)^2). */
+static int64_t nearest_sqrt(int64_t f) {
+  int64_t n = 0;
+  while ((n + 1) * (n + 1) <= f) n++;
+  return f > n * n + n ? n + 1 : n;
+}
+
+/* The paper tracks each rank's sending volume under the replication plan,
+ * then, one hot expert at a time, picks first-stage relays among the
+ * expert's replica ranks with the smallest volume and hangs every other
+ * replica under the relay whose volume stays smallest after taking it; the
+ * source's and relays' volumes are updated before the next expert.
+ * Readings where the text is open:
+ *   - eligible: replica count f_e = |H(e)| - 1 exceeds `threshold` (4 in
+ *     the paper);
+ *   - frontier: n_e = the integer nearest sqrt(f_e);
+ *   - volume unit: one expert blob (all experts of a layer have the same
+ *     size); rank r starts with one blob per replica of each main expert;
+ *   - hot experts in order of f_e descending, then e ascending;
+ *   - relays: the n_e replica ranks of smallest volume, ties to the smaller
+ *     rank;
+ *   - leaves: the other replicas by ascending rank, each under the relay of
+ *     smallest volume (ties to the smaller rank), whose volume grows by one
+ *     at once;
+ *   - after the expert's leaves, the source's volume drops by f_e - n_e.
+ * Output: slot_src[t*n_slot + s] = the rank that sends the blob of redundant
+ * slot (t, s) (the home rank or a relay), -1 for an empty slot; send_vol[r];
+ * relay_stats = {relay experts, sum of n_e, max volume before, max volume
+ * after}. */
+int orc_relay(const orc_group *g, const int32_t *slot_expert,
+              const int32_t *host_ptr, const int32_t *host_rank,
+              const int32_t *host_pslot, int32_t threshold, int32_t *slot_src,
+              int32_t *send_vol, int64_t *relay_stats) {
+  if (!group_ok(g) || !host_ptr || !host_rank || !host_pslot || threshold < 0 ||
+      !send_vol || !relay_stats || (g->n_slot > 0 && (!slot_expert || !slot_src)))
+    return ORC_EINVAL;
+  const int32_t R = g->R, E = g->E, NS = g->n_slot, nm = E / R;
+  const int64_t ncol = (int64_t)E + (int64_t)R * NS;
+  /* the CSR must describe the slot map: home first, then replicas by
+   * ascending rank, each on the slot that holds the expert */
+  if (host_ptr[0] != 0 || host_ptr[E] < E || host_ptr[E] > ncol) return ORC_EDATA;
+  for (int32_t e = 0; e < E; e++) {
+    int32_t j0 = host_ptr[e], j1 = host_ptr[e + 1];
+    if (j1 <= j0 || host_rank[j0] != home(g, e) || host_pslot[j0] != e - home(g, e) * nm)
+      return ORC_EDATA;
+    for (int32_t j = j0 + 1; j < j1; j++) {
+      int32_t t = host_rank[j], s = host_pslot[j] - nm;
+      if (t < 0 || t >= R || s < 0 || s >= NS || slot_expert[(int64_t)t * NS + s] != e ||
+          (j > j0 + 1 && t <= host_rank[j - 1]) || t == home(g, e))
+        return ORC_EDATA;
+    }
+  }
+  int64_t *vol = calloc((size_t)R, sizeof(int64_t));
+  for (int32_t t = 0; t < R; t++)
+    for (int32_t s = 0; s < NS; s++) {
+      int32_t e = slot_expert[(int64_t)t * NS + s];
+      slot_src[(int64_t)t * NS + s] = e >= 0 ? home(g, e) : -1;
+      if (e >= 0) vol[home(g, e)] += 1;
+    }
+  int64_t vmax0 = 0;
+  for (int32_t r = 0; r < R; r++) vmax0 = max64(vmax0, vol[r]);
+
+  /* hot experts, by replica count descending, then id ascending */
+  int32_t *hot = malloc(sizeof(int32_t) * (size_t)E);
+  int32_t nhot = 0;
+  for (int32_t e = 0; e < E; e++)
+    if (host_ptr[e + 1] - host_ptr[e] - 1 > threshold) hot[nhot++] = e;
+  for (int32_t a = 1; a < nhot; a++) { /* insertion sort */
+    int32_t e = hot[a], fe = host_ptr[e + 1] - host_ptr[e] - 1, b = a;
+    while (b > 0) {
+      int32_t p = hot[b - 1], fp = host_ptr[p + 1] - host_ptr[p] - 1;
+      if (fp > fe || (fp == fe && p < e)) break;
+      hot[b] = p;
+      b--;
+    }
+    hot[b] = e;
+  }
+
+  int64_t n_relays = 0;
+  int32_t *is_relay = calloc((size_t)R, sizeof(int32_t));
+  for (int32_t h = 0; h < nhot; h++) {
+    int32_t e = hot[h], j0 = host_ptr[e], j1 = host_ptr[e + 1];
+    int64_t f = j1 - j0 - 1, n = nearest_sqrt(f);
+    for (int32_t r = 0; r < R; r++) is_relay[r] = 0;
+    /* first-stage relays: smallest volume, ties to the smaller rank */
+    for (int64_t i = 0; i < n; i++) {
+      int32_t best = -1;
+      for (int32_t j = j0 + 1; j < j1; j++) {
+        int32_t t = host_rank[j];
+        if (is_relay[t]) continue;
+        if (best < 0 || vol[t] < vol[best] || (vol[t] == vol[best] && t < best)) best = t;
+      }
+      is_relay[best] = 1;
+    }
+    /* leaves, ascending rank: the relay whose volume stays smallest */
+    for (int32_t j = j0 + 1; j < j1; j++) {
+      int32_t t = host_rank[j];
+      if (is_relay[t]) continue;
+      int32_t best = -1;
+      for (int32_t jr = j0 + 1; jr < j1; jr++) {
+        int32_t u = host_rank[jr];
+        if (!is_relay[u]) continue;
+        if (best < 0 || vol[u] + 1 < vol[best] + 1 || (vol[u] == vol[best] && u < best)) best = u;
+      }
+      vol[best] += 1;
+      slot_src[(int64_t)t * NS + (host_pslot[j] - nm)] = best;
+    }
+    vol[home(g, e)] -= f - n; /* the source now sends to its relays only */
+    n_relays += n;
+  }
+  int64_t vmax1 = 0;
+  for (int32_t r = 0; r < R; r++) {
+    vmax1 = max64(vmax1, vol[r]);
+    send_vol[r] = (int32_t)vol[r];
+  }
+  relay_stats[0] = nhot;
+  relay_stats[1] = n_relays;
+  relay_stats[2] = vmax0;
+  relay_stats[3] = vmax1;
+  free(vol);
+  free(hot);
+  free(is_relay);
+  return ORC_OK;
+}
+
+/* Local half of the weight distribution with relay trees: rank `rank`
+ * stages one copy for every redundant slot whose sender (slot_src) it is,
+ * destination ascending then slot ascending.  The blob of its own main
+ * expert comes from w_main; the blob of an expert it relays comes from its
+ * own redundant slot holding that expert (relay_src[s], the buffer the
+ * first stage fills). */
+int orc_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W,
+                   int32_t rank, const orc_group *g, const int32_t *slot_expert,
+                   const int32_t *slot_src, uint16_t *staging, int64_t cap,
+                   int64_t *dest_off, int64_t *n_out) {
+  if (!group_ok(g) || W < 1 || rank < 0 || rank >= g->R || !dest_off || !n_out ||
+      cap < 0 || !w_main || (g->n_slot > 0 && (!slot_expert || !slot_src)))
+    return ORC_EINVAL;
+  const int32_t R = g->R, NS = g->n_slot, nm = g->E / g->R;
+  int64_t n = 0;
+  for (int32_t t = 0; t < R; t++) {
+    dest_off[t] = n;
+    for (int32_t s = 0; s < NS; s++)
+      if (slot_expert[(int64_t)t * NS + s] >= 0 && slot_src[(int64_t)t * NS + s] == rank) n++;
+  }
+  dest_off[R] = n;
+  *n_out = n;
+  if (n > cap) return ORC_ENOSPC;
+  if (n > 0 && !staging) return ORC_EINVAL;
+  n = 0;
+  for (int32_t t = 0; t < R; t++)
+    for (int32_t s = 0; s < NS; s++) {
+      int32_t e = slot_expert[(int64_t)t * NS + s];
+      if (e < 0 || slot_src[(int64_t)t * NS + s] != rank) continue;
+      const uint16_t *src = NULL;
+      if (home(g, e) == rank) {
+        src = w_main + (int64_t)(e - rank * nm) * W;
+      } else {
+        for (int32_t s2 = 0; s2 < NS; s2++)
+          if (slot_expert[(int64_t)rank * NS + s2] == e) src = relay_src + (int64_t)s2 * W;
+        if (!src || !relay_src) return ORC_EDATA; /* relays an expert it does not host */
+      }
+      memcpy(staging + n * W, src, sizeof(uint16_t) * (size_t)W);
+      n++;
+    }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------ */
 /* Diagnostics — Eqs. (3)-(5) and Table 3                             */
 /* ------------------------------------------------------------------ */
 

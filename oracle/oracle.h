@@ -84,6 +84,22 @@ int orc_pack(const uint16_t *w_main, int64_t W, int32_t rank,
              uint16_t *staging, int64_t cap, int64_t *dest_off,
              int64_t *n_out);
 
+/* Relay trees for experts with more than `threshold` replicas (Sec. 6.2):
+ * slot_src[R][n_slot] = the rank sending each redundant slot's blob (-1:
+ * empty slot), send_vol[R] = blobs each rank sends, relay_stats[4] = relay
+ * experts, relays, max volume before, max volume after. */
+int orc_relay(const orc_group *g, const int32_t *slot_expert,
+              const int32_t *host_ptr, const int32_t *host_rank,
+              const int32_t *host_pslot, int32_t threshold, int32_t *slot_src,
+              int32_t *send_vol, int64_t *relay_stats);
+
+/* Pack with relay trees: one copy per redundant slot whose sender is `rank`;
+ * relayed blobs come from relay_src[n_slot][W] (this rank's own slots). */
+int orc_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W,
+                   int32_t rank, const orc_group *g, const int32_t *slot_expert,
+                   const int32_t *slot_src, uint16_t *staging, int64_t cap,
+                   int64_t *dest_off, int64_t *n_out);
+
 /* Diagnostics of a plan: out[0..5] = max rank load before, mean load (x1),
  * max rank load after, n_replicas, max |H(e)|, remote (in-flight) tokens. */
 int orc_metrics(const int32_t *load, const orc_group *g,

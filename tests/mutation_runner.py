@@ -11,6 +11,7 @@ import gen  # noqa: E402
 import oracle  # noqa: E402
 import test_oracle_invariants as inv  # noqa: E402
 import test_oracle_pins as pins  # noqa: E402
+import test_oracle_relay as relay  # noqa: E402
 
 
 def main(lib_path, bf_exe):
@@ -31,6 +32,14 @@ def main(lib_path, bf_exe):
         lambda: [pins.test_s3_single_hot_expert_closed_form(orc, R) for R in (2, 5)],
         lambda: pins.test_bruteforce_small_random_groups(orc, bf_exe),
         lambda: [inv.test_fuzz_case(orc, s) for s in range(40)],
+        lambda: relay.test_figure_nine_replicas_three_relays(),
+        lambda: [relay.test_single_hot_expert_closed_form(f, n)
+                 for f, n in sorted(relay.FRONTIER.items())],
+        lambda: [relay.test_at_most_four_replicas_no_relay(f) for f in (1, 4)],
+        lambda: relay.test_relays_avoid_busy_senders(),
+        lambda: relay.test_second_hot_expert_sees_first_ones_volumes(),
+        lambda: relay.test_larger_fanout_goes_first(),
+        lambda: relay.test_pack_relay_stages_for_the_slots_a_rank_sends(),
     ]
     for i, chk in enumerate(checks):
         try:

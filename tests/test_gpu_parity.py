@@ -131,6 +131,26 @@ def test_full_size_dispatch_and_pack(cid, m):
         gp.check_rank(x, tk[r], w, r, g, og, plan, op, split=(r == rs[-1]))
 
 
+@pytest.mark.parametrize("H", [520, 1032, 2056, 7176, 8192, 8200, 16400])
+def test_scatter_row_widths(H):
+    """Row widths for every register tiling of the scatter (16-byte chunks per
+    lane 2, 4, 8, 16, and the multi-pass kernel above 8192 elements), with
+    more tokens than the resident waves (each wave walks several tokens) and
+    a quarter of the slots masked (zero-filled tail rows)."""
+    R, E, NS, k, T = 4, 16, 2, 2, 2100
+    g, og = gp.groups(R, E, NS, 8)
+    rng = np.random.default_rng(H)
+    tk = rng.integers(0, E, (R, T, k)).astype(np.int32)
+    tk[rng.random((R, T, k)) < 0.25] = -1
+    load, _ = oracle.count(tk, E, R)
+    op = oracle.plan(load, og)
+    plan = gp.gpu_plan(load, g)
+    gp.assert_plan_equal(plan, op)
+    r = 1
+    x = rng.integers(0, 1 << 16, (T, H)).astype(np.uint16)
+    gp.check_rank(x, tk[r], None, r, g, og, plan, op, split=True)
+
+
 @pytest.mark.parametrize("seed", range(0, 160))
 def test_fuzz_parity(seed):
     case = fuzz.make_case(seed)

@@ -46,6 +46,21 @@ MUTATIONS = {
     "residual_not_updated": ("        uhat[i] -= qv[i];\n", "\n"),
     "home_keeps_nothing_back": ("Ut[(int64_t)e * R + home(g, e)] -= delta;",
                                 "Ut[(int64_t)e * R + home(g, e)] -= 0;"),
+    "relay_threshold_inclusive": (
+        "if (host_ptr[e + 1] - host_ptr[e] - 1 > threshold) hot[nhot++] = e;",
+        "if (host_ptr[e + 1] - host_ptr[e] - 1 >= threshold) hot[nhot++] = e;"),
+    "relay_frontier_floor": ("return f > n * n + n ? n + 1 : n;", "return n;"),
+    "relay_hot_order_ascending": ("if (fp > fe || (fp == fe && p < e)) break;",
+                                  "if (fp < fe || (fp == fe && p < e)) break;"),
+    "relay_picks_largest_volume": (
+        "if (best < 0 || vol[t] < vol[best] || (vol[t] == vol[best] && t < best)) best = t;",
+        "if (best < 0 || vol[t] > vol[best] || (vol[t] == vol[best] && t < best)) best = t;"),
+    "relay_leaf_tie_to_larger_rank": (
+        "if (best < 0 || vol[u] + 1 < vol[best] + 1 || (vol[u] == vol[best] && u < best)) best = u;",
+        "if (best < 0 || vol[u] + 1 <= vol[best] + 1) best = u;"),
+    "relay_leaf_volume_not_counted": ("      vol[best] += 1;\n      slot_src", "      slot_src"),
+    "relay_source_not_updated": ("vol[home(g, e)] -= f - n;", "vol[home(g, e)] -= 0;"),
+    "pack_relay_reads_main_blob": ("src = relay_src + (int64_t)s2 * W;", "src = w_main;"),
 }
 
 
