@@ -10,6 +10,8 @@
  *   4. ultraep_pack_replicas  local half of weight distribution: the blobs of
  *                             this rank's replicated main experts copied into
  *                             per-destination staging
+ *      ultraep_relay_plan     relay trees for hot-expert fan-out, and
+ *      ultraep_pack_relay     the packing that follows them
  *
  * Conventions for every call:
  *   - Buffer pointers are DEVICE pointers unless marked "host".  The caller
@@ -220,6 +222,45 @@ int ultraep_reroute_and_pack(const int32_t *load, const ultraep_group *g,
                              const ultraep_plan_buf *plan, const uint16_t *w_main, int64_t W,
                              int32_t rank, uint16_t *staging, int64_t cap, int64_t *dest_off,
                              int32_t *status, hipStream_t stream);
+
+/* Relay trees for hot-expert fan-out (Sec. 6.2, load-aware relay
+ * scheduling), from a plan (slot_expert and the host lists).  Each rank's
+ * sending volume starts at one expert blob per replica of its main experts.
+ * Every expert with more than `threshold` replicas (the paper uses 4), by
+ * replica count descending then id ascending, gets the integer nearest
+ * sqrt(replicas) first-stage relays: its replica ranks of smallest volume;
+ * each other replica, by ascending rank, is served by the relay whose
+ * volume is smallest (one blob added at once); the source's volume then
+ * drops to one blob per relay.  Ties go to the smaller rank.
+ *   threshold    >= 0
+ *   slot_src     [R * n_slot] int32: the rank that sends redundant slot
+ *                (t, s) its blob (the expert's home rank or a relay), -1 for
+ *                an empty slot
+ *   send_vol     [R] int32: blobs each rank sends under the trees
+ *   relay_stats  [4] int64: experts with relays, relays in total, largest
+ *                sending volume before and after
+ * A plan whose host lists do not match its slot map, or whose stats[6] is
+ * nonzero, raises ULTRAEP_EDATA (outputs undefined).  Every output element
+ * is written otherwise. */
+int ultraep_relay_plan(const ultraep_group *g, const ultraep_plan_buf *plan, int32_t threshold,
+                       int32_t *slot_src, int32_t *send_vol, int64_t *relay_stats,
+                       int32_t *status, hipStream_t stream);
+
+/* Local half of the weight distribution with relay trees (Sec. 6.1 tile
+ * copy, Sec. 6.2 trees): every redundant slot (t, s) whose sender
+ * slot_src[t * n_slot + s] is `rank` receives a bit copy of its expert's
+ * blob, entries ordered by destination rank t, then slot s.  The blob of a
+ * main expert of `rank` comes from w_main; the blob of an expert that
+ * `rank` relays comes from relay_src[s'], this rank's own redundant slot s'
+ * holding that expert (the buffer the first stage fills).
+ *   relay_src  [n_slot][W] bf16 (needed when n_slot > 0)
+ *   staging, dest_off, cap as for ultraep_pack_replicas.
+ * A slot this rank should relay without hosting its expert raises
+ * ULTRAEP_EDATA; n_out > cap raises ULTRAEP_ENOSPC. */
+int ultraep_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W, int32_t rank,
+                       const ultraep_group *g, const ultraep_plan_buf *plan,
+                       const int32_t *slot_src, uint16_t *staging, int64_t cap,
+                       int64_t *dest_off, int32_t *status, hipStream_t stream);
 
 /* Host only.  Static description of a status code. */
 const char *ultraep_strerror(int code);

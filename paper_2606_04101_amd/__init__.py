@@ -93,13 +93,17 @@ def lib():
                                             _P, _P]
         L.ultraep_reroute_and_pack.argtypes = [_P, gp, pp, _P, i64, i32, _P, i64, _P,
                                                _P, _P]
+        L.ultraep_relay_plan.argtypes = [gp, pp, i32, _P, _P, _P, _P, _P]
+        L.ultraep_pack_relay.argtypes = [_P, _P, i64, i32, gp, pp, _P, _P, i64, _P,
+                                         _P, _P]
         L.ultraep_strerror.argtypes = [ctypes.c_int]
         L.ultraep_strerror.restype = ctypes.c_char_p
         for f in ("ultraep_plan_sizes", "ultraep_count", "ultraep_plan",
                   "ultraep_plan_replicate", "ultraep_plan_reroute",
                   "ultraep_dispatch", "ultraep_dispatch_layout",
                   "ultraep_dispatch_scatter", "ultraep_pack_replicas",
-                  "ultraep_reroute_and_pack"):
+                  "ultraep_reroute_and_pack", "ultraep_relay_plan",
+                  "ultraep_pack_relay"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -231,6 +235,22 @@ def ultraep_reroute_and_pack(load, g: Group, plan: Plan, w_main, W, rank, stagin
         _ptr(load), ctypes.byref(g), ctypes.byref(plan.c), _ptr(w_main), W, rank,
         _ptr(staging), cap, _ptr(dest_off), _ptr(status), _stream(stream)),
         "ultraep_reroute_and_pack")
+
+
+def ultraep_relay_plan(g: Group, plan: Plan, threshold, slot_src, send_vol,
+                       relay_stats, status, stream=None):
+    return _check(lib().ultraep_relay_plan(
+        ctypes.byref(g), ctypes.byref(plan.c), threshold, _ptr(slot_src),
+        _ptr(send_vol), _ptr(relay_stats), _ptr(status), _stream(stream)),
+        "ultraep_relay_plan")
+
+
+def ultraep_pack_relay(w_main, relay_src, W, rank, g: Group, plan: Plan, slot_src,
+                       staging, cap, dest_off, status, stream=None):
+    return _check(lib().ultraep_pack_relay(
+        _ptr(w_main), _ptr(relay_src), W, rank, ctypes.byref(g), ctypes.byref(plan.c),
+        _ptr(slot_src), _ptr(staging), cap, _ptr(dest_off), _ptr(status),
+        _stream(stream)), "ultraep_pack_relay")
 
 
 def build():

@@ -8,7 +8,8 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libultraep.so")
-SOURCES = ["abi.hip", "count.hip", "plan.hip", "dispatch.hip", "pack.hip"]
+SOURCES = ["abi.hip", "count.hip", "plan.hip", "dispatch.hip", "pack.hip",
+           "relay.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # packed fp32 instructions are disabled for all device code

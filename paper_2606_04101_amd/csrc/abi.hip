@@ -153,6 +153,27 @@ int ultraep_reroute_and_pack(const int32_t *load, const ultraep_group *g,
                                      status, stream));
 }
 
+int ultraep_relay_plan(const ultraep_group *g, const ultraep_plan_buf *plan, int32_t threshold,
+                       int32_t *slot_src, int32_t *send_vol, int64_t *relay_stats,
+                       int32_t *status, hipStream_t stream) {
+  if (!group_ok(g) || !plan_ok(g, plan) || threshold < 0) return ULTRAEP_EINVAL;
+  if (!send_vol || !relay_stats || !status || (g->n_slot > 0 && !slot_src)) return ULTRAEP_EINVAL;
+  return rc(uep::launch_relay(*g, *plan, threshold, slot_src, send_vol, relay_stats, status,
+                              stream));
+}
+
+int ultraep_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W, int32_t rank,
+                       const ultraep_group *g, const ultraep_plan_buf *plan,
+                       const int32_t *slot_src, uint16_t *staging, int64_t cap,
+                       int64_t *dest_off, int32_t *status, hipStream_t stream) {
+  if (!group_ok(g) || !plan_ok(g, plan) || rank < 0 || rank >= g->R) return ULTRAEP_EINVAL;
+  if (W < 8 || W % 8 != 0 || cap < 0 || !dest_off || !status || !w_main) return ULTRAEP_EINVAL;
+  if (g->n_slot > 0 && (!slot_src || !relay_src || !aligned16(relay_src))) return ULTRAEP_EINVAL;
+  if (!aligned16(w_main) || (cap > 0 && (!staging || !aligned16(staging)))) return ULTRAEP_EINVAL;
+  return rc(uep::launch_pack_relay(w_main, relay_src, W, rank, *g, *plan, slot_src, staging, cap,
+                                   dest_off, status, stream));
+}
+
 const char *ultraep_strerror(int code) {
   switch (code) {
     case ULTRAEP_OK: return "ok";

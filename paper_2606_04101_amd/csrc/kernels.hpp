@@ -56,4 +56,14 @@ hipError_t launch_pack(const uint16_t *w_main, int64_t W, int32_t rank,
                        uint16_t *staging, int64_t cap, int64_t *dest_off,
                        int32_t *status, hipStream_t stream);
 
+hipError_t launch_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W,
+                             int32_t rank, const ultraep_group &g, const ultraep_plan_buf &plan,
+                             const int32_t *slot_src, uint16_t *staging, int64_t cap,
+                             int64_t *dest_off, int32_t *status, hipStream_t stream);
+
+// relay trees of the hot experts (one workgroup)
+hipError_t launch_relay(const ultraep_group &g, const ultraep_plan_buf &plan, int32_t threshold,
+                        int32_t *slot_src, int32_t *send_vol, int64_t *stats, int32_t *status,
+                        hipStream_t stream);
+
 }  // namespace uep

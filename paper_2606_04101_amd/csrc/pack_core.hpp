@@ -15,7 +15,14 @@
 // non-temporal stores, so every source byte is read once; the experts
 // interleave so hot and cold ones spread over all workgroups.
 //
-// Used by k_pack and by the kernel that runs it alongside SolveReroute.
+// With relay trees (Sec. 6.2) a rank sends the slots whose sender it is:
+// its own main experts' blobs to their relays and direct replicas, and the
+// blobs it holds as a relay (its own redundant slot, filled by the first
+// stage) to its leaves.  The groups are then numbered by source: main
+// expert l < n_main, or the rank's redundant slot n_main + s.
+//
+// Used by k_pack, by the kernel that runs it alongside SolveReroute, and
+// (RELAY) by k_pack_relay.
 #pragma once
 
 #include "common.hpp"
@@ -28,14 +35,16 @@ constexpr int kPkWaves = kPkThreads / kWave;
 constexpr int kPkUnroll = 4;                        // v4u per thread per tile
 constexpr int kPkTileCh = kPkThreads * kPkUnroll;   // 1024 x 16 B = 16 KiB
 constexpr int kPkMaxEnt = 256;                      // R * n_slot
-constexpr int kPkMaxLocal = 1024;                   // main experts per rank
+constexpr int kPkMaxLocal = 1024 + 256;             // main experts + redundant slots
 constexpr int kPkGrid = 4096;  // about one tile per workgroup at these sizes
 
 struct PkArgs {
   const v4u *w;
+  const v4u *relay_src;    // RELAY: this rank's redundant-slot blobs [NS][nch]
   int64_t nch;  // 16-byte chunks per expert blob
   int32_t rank, R, NS, nm;
   const int32_t *X;
+  const int32_t *slot_src;  // RELAY: sender rank of every redundant slot
   v4u *staging;
   int64_t cap;
   int64_t *dest_off;
@@ -43,7 +52,9 @@ struct PkArgs {
 };
 
 // Workgroup wg of n_wg runs its share of the tasks; the one with writes_meta
-// also writes dest_off and reports a capacity overflow.
+// also writes dest_off and reports a capacity overflow (and, RELAY, a slot
+// this rank should relay without hosting its expert).
+template <bool RELAY = false>
 __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t n_wg,
                                            bool writes_meta) {
   __shared__ int32_t s_dst[kPkMaxEnt];         // destination entries, grouped by expert
@@ -55,12 +66,25 @@ __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t 
 
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int RS = a.R * a.NS;
-  for (int l = tid; l < a.nm; l += kPkThreads) s_cnt[l] = 0;
+  const int nsrc = RELAY ? a.nm + a.NS : a.nm;  // source blobs
+  for (int l = tid; l < nsrc; l += kPkThreads) s_cnt[l] = 0;
   int li = -1;
+  bool orphan = false;
   if (tid < RS) {
     const int e = a.X[tid];
-    if (e >= 0 && e / a.nm == a.rank) li = e - a.rank * a.nm;
+    if (!RELAY) {
+      if (e >= 0 && e / a.nm == a.rank) li = e - a.rank * a.nm;
+    } else if (e >= 0 && a.slot_src[tid] == a.rank) {
+      if (e / a.nm == a.rank) {
+        li = e - a.rank * a.nm;
+      } else {  // relayed: the first stage filled this rank's slot holding e
+        for (int s2 = 0; s2 < a.NS; ++s2)
+          if (a.X[a.rank * a.NS + s2] == e) li = a.nm + s2;
+        orphan = li < 0;
+      }
+    }
   }
+  if (RELAY && orphan && writes_meta) report(a.status, ULTRAEP_EDATA);
   const bool valid = li >= 0;
   const uint64_t bv = ballot(valid);
   if (lane == 0) s_wcnt[wave] = __popcll(bv);
@@ -96,9 +120,9 @@ __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t 
   if (fidx == 0) s_gstart[li] = atomicAdd(&s_off, s_cnt[li]);
   // the groups themselves in ascending local-expert order, the same in
   // every workgroup, since tasks are numbered by group
-  for (int l0 = 0; l0 < a.nm; l0 += kPkThreads) {
+  for (int l0 = 0; l0 < nsrc; l0 += kPkThreads) {
     const int l = l0 + tid;
-    const bool has = l < a.nm && s_cnt[l] > 0;
+    const bool has = l < nsrc && s_cnt[l] > 0;
     const uint64_t hb = ballot(has);
     int gi = s_ngrp + popc_below(hb);
     __syncthreads();
@@ -121,7 +145,8 @@ __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t 
   for (int64_t task = wg; task < ntask; task += n_wg) {
     const int l = s_gli[static_cast<int>(task % ngrp)];
     const int64_t c0 = (task / ngrp) * kPkTileCh;
-    const v4u *src = a.w + static_cast<int64_t>(l) * a.nch;
+    const v4u *src = !RELAY || l < a.nm ? a.w + static_cast<int64_t>(l) * a.nch
+                                        : a.relay_src + static_cast<int64_t>(l - a.nm) * a.nch;
     v4u v[kPkUnroll];
 #pragma unroll
     for (int u = 0; u < kPkUnroll; ++u) {
@@ -145,6 +170,8 @@ inline PkArgs pack_args(const uint16_t *w_main, int64_t W, int32_t rank,
                         uint16_t *staging, int64_t cap, int64_t *dest_off, int32_t *status) {
   PkArgs a;
   a.w = reinterpret_cast<const v4u *>(w_main);
+  a.relay_src = nullptr;
+  a.slot_src = nullptr;
   a.nch = W / 8;
   a.rank = rank;
   a.R = g.R;

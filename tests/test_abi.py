@@ -24,7 +24,8 @@ def test_header_declares_the_entry_points():
               "ultraep_plan_replicate", "ultraep_plan_reroute", "ultraep_reroute_and_pack",
               "ultraep_dispatch_layout", "ultraep_dispatch_scatter",
               "ultraep_pack_replicas", "ultraep_plan_sizes",
-              "ultraep_dispatch_ws_bytes", "ultraep_strerror"):
+              "ultraep_dispatch_ws_bytes", "ultraep_strerror",
+              "ultraep_relay_plan", "ultraep_pack_relay"):
         assert n in names
 
 
@@ -108,6 +109,21 @@ def test_invalid_arguments_return_einval_without_launch():
                                    fake, -1, fake, fake, None) == E    # cap < 0
     assert L.ultraep_pack_replicas(fake, 16, 0, ctypes.byref(g), ctypes.byref(full),
                                    odd, 4, fake, fake, None) == E      # misaligned
+
+    # relay trees: negative threshold, missing outputs, bad group or plan
+    for gg, pl, thr, src, vol, st in [(g, full, -1, fake, fake, fake), (bad, full, 4, fake, fake, fake),
+                                      (g, pb, 4, fake, fake, fake), (g, full, 4, None, fake, fake),
+                                      (g, full, 4, fake, None, fake), (g, full, 4, fake, fake, None)]:
+        assert L.ultraep_relay_plan(ctypes.byref(gg), ctypes.byref(pl), thr, src, vol, fake, st,
+                                    None) == E
+    for w, rs, W, rank, src, stg in [(fake, None, 16, 0, fake, fake),   # no relay source
+                                     (fake, odd, 16, 0, fake, fake),    # misaligned relay source
+                                     (fake, fake, 12, 0, fake, fake),   # W % 8
+                                     (fake, fake, 16, 4, fake, fake),   # rank >= R
+                                     (fake, fake, 16, 0, None, fake),   # no slot senders
+                                     (None, fake, 16, 0, fake, fake)]:  # no blobs
+        assert L.ultraep_pack_relay(w, rs, W, rank, ctypes.byref(g), ctypes.byref(full), src,
+                                    stg, 4, fake, fake, None) == E
 
 
 def test_strerror():
