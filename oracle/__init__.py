@@ -25,8 +25,10 @@ OK, EINVAL, ENOSPC, EDATA, ELEMMA = 0, -1, -2, -4, -6
 
 def build() -> str:
     """Compile ``liboracle.so`` with gcc (-O2, C11, no GPU headers)."""
-    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared",
-           "-o", _LIB + ".tmp", _SRC]
+    # -ffp-contract=off: no fused multiply-add in the fp32 combine and
+    # reduction (each product and sum rounds on its own)
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off",
+           "-fPIC", "-shared", "-o", _LIB + ".tmp", _SRC]
     subprocess.run(cmd, check=True, cwd=_HERE)
     os.replace(_LIB + ".tmp", _LIB)
     return _LIB
@@ -85,9 +87,11 @@ def _load(path):
     L.orc_metrics.argtypes = [_P, gp, _P, _P, _P, _P, _P]
     L.orc_relay.argtypes = [gp, _P, _P, _P, _P, i32, _P, _P, _P]
     L.orc_pack_relay.argtypes = [_P, _P, i64, i32, gp, _P, _P, _P, i64, _P, _P]
+    L.orc_combine.argtypes = [_P, _P, _P, i64, i32, i32, i64, _P]
+    L.orc_grad_reduce.argtypes = [_P, _P, i64, i32, gp, _P, i64, _P]
     for f in ("orc_count", "orc_probe", "orc_plan", "orc_bisect_trace",
               "orc_apportion", "orc_dispatch", "orc_pack", "orc_metrics",
-              "orc_relay", "orc_pack_relay"):
+              "orc_relay", "orc_pack_relay", "orc_combine", "orc_grad_reduce"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -270,6 +274,34 @@ def pack_relay(w_main, relay_src, rank, g: Group, slot_expert, slot_src, cap):
                               _p(staging) if staging.size else None, cap, _p(doff),
                               _p(n_out))
     return staging, doff, int(n_out[0]), st
+
+
+def combine(y, gate, row_of_slot):
+    """-> out [T, H] uint16 (bf16 bits), status.  y [n_rows, H] uint16,
+    gate [T, k] float32, row_of_slot [T*k] or [T, k] int32."""
+    y = _c(y, np.uint16)
+    gate = _c(gate, np.float32)
+    T, k = gate.shape
+    ros = _c(row_of_slot, np.int32).reshape(-1)
+    n_rows, H = y.shape
+    out = np.zeros((T, H), np.uint16)
+    st = lib().orc_combine(_p(y) if y.size else None, _p(gate), _p(ros), T, k, H, n_rows,
+                           _p(out))
+    return out, st
+
+
+def grad_reduce(main_grad, rgrad, rank, g: Group, slot_expert, cap):
+    """In place on copies: -> (main_grad', rgrad', n_out, status)."""
+    mg = np.array(main_grad, dtype=np.float32, copy=True, order="C")
+    rg = np.array(rgrad, dtype=np.float32, copy=True, order="C")
+    W = mg.shape[1]
+    n_out = np.zeros(1, np.int64)
+    gc = g.c()
+    X = _c(slot_expert, np.int32).reshape(-1)
+    st = lib().orc_grad_reduce(_p(mg), _p(rg) if rg.size else None, W, rank,
+                               ctypes.byref(gc), _p(X) if X.size else _p(np.zeros(1, np.int32)),
+                               cap, _p(n_out))
+    return mg, rg, int(n_out[0]), st
 
 
 def metrics(load, g: Group, p: Plan):

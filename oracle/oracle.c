@@ -10,7 +10,8 @@
  *   - Sec. 4.1 (main / redundant slot layout) and Sec. 6.1 (weight tiles)
  *   - Eqs. (3)-(5) and Table 3 (diagnostic metrics)
  * Where the paper is silent the reading used is stated inline; the same
- * readings bind the HIP library.  Only the test-suite, the smoke check and the
+ * readings bind the HIP library.  Floating point appears only in the
+ * combine gather and the gradient reduction, in fp32 with a fixed order.  Only the test-suite, the smoke check and the
  * benchmark's CPU-baseline leg may load this code.
  */
 #include "oracle.h"
@@ -715,6 +716,107 @@ int orc_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W,
         if (!src || !relay_src) return ORC_EDATA; /* relays an expert it does not host */
       }
       memcpy(staging + n * W, src, sizeof(uint16_t) * (size_t)W);
+      n++;
+    }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Reverse reroute: combine gather (Sec. 4.2 backward / the inverse   */
+/* of the token assignment).  The ONLY floating point in the oracle.  */
+/* ------------------------------------------------------------------ */
+
+/* bf16 <-> fp32.  A bf16 pattern is the upper half of an fp32 pattern, so
+ * widening is exact.  Narrowing rounds to nearest, ties to even: keep the
+ * upper 16 bits, and add one unit of the kept part when the dropped 16 bits
+ * exceed half a unit, or equal half a unit with an odd kept part.  NaNs
+ * become the quiet NaN 0x7FC0 (sign kept). */
+static float bf16_to_f32(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+static uint16_t f32_to_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  uint32_t sign = u & 0x80000000u, mag = u & 0x7FFFFFFFu;
+  if (mag > 0x7F800000u) return (uint16_t)((sign >> 16) | 0x7FC0u); /* NaN */
+  uint32_t kept = u >> 16, dropped = u & 0xFFFFu;
+  if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1; /* may carry into the exponent: correct, up to inf */
+  return (uint16_t)kept;
+}
+
+/* Reading of the combine's arithmetic (the paper fixes bf16 activations
+ * only): out[t] = bf16( sum over k ascending of fp32(gate[t][kk] * y[row]) )
+ * with the sum accumulated in fp32 from +0, each product and each partial
+ * sum rounded to fp32 (no fused multiply-add), masked slots (row -1)
+ * skipped.  y is [n_rows][H] bf16 in the dispatch layout (row_of_slot),
+ * gate [T][k] fp32, out [T][H] bf16.  A row outside [0, n_rows) is
+ * ORC_EDATA. */
+int orc_combine(const uint16_t *y, const float *gate, const int32_t *row_of_slot,
+                int64_t T, int32_t k, int32_t H, int64_t n_rows, uint16_t *out) {
+  if (T < 0 || k < 1 || H < 1 || n_rows < 0) return ORC_EINVAL;
+  if (T > 0 && (!gate || !row_of_slot || !out)) return ORC_EINVAL;
+  if (n_rows > 0 && !y) return ORC_EINVAL;
+  for (int64_t i = 0; i < T * k; i++)
+    if (row_of_slot[i] < -1 || row_of_slot[i] >= n_rows) return ORC_EDATA;
+  for (int64_t t = 0; t < T; t++)
+    for (int32_t h = 0; h < H; h++) {
+      volatile float acc = 0.0f; /* volatile: every partial sum is an fp32 value */
+      for (int32_t kk = 0; kk < k; kk++) {
+        int32_t row = row_of_slot[t * k + kk];
+        if (row < 0) continue;
+        volatile float prod = gate[t * k + kk] * bf16_to_f32(y[(int64_t)row * H + h]);
+        acc = acc + prod;
+      }
+      out[t * H + h] = f32_to_bf16(acc);
+    }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Gradient reduction, local half (Sec. 4.2 backward, Sec. 6.1)       */
+/* ------------------------------------------------------------------ */
+
+/* The gradients of this rank's replicated main experts come back from
+ * their replicas and are accumulated into the main gradients, then the
+ * replica buffers are cleared for the next layer.  Gradients are fp32 (the
+ * paper's redundant-slot gradient is twice its bf16 weight).  Readings:
+ * rgrad holds one [W] fp32 blob per replica, in the staging order of the
+ * forward packing (destination rank ascending, then slot); each main
+ * gradient is summed in fp32 starting from its own value and adding its
+ * replicas in that order; every rgrad entry is zeroed afterwards.
+ * ORC_ENOSPC if this rank has more replicas than cap (nothing changes). */
+int orc_grad_reduce(float *main_grad, float *rgrad, int64_t W, int32_t rank,
+                    const orc_group *g, const int32_t *slot_expert, int64_t cap,
+                    int64_t *n_out) {
+  if (!group_ok(g) || W < 1 || rank < 0 || rank >= g->R || !main_grad || !n_out || cap < 0 ||
+      (g->n_slot > 0 && !slot_expert))
+    return ORC_EINVAL;
+  const int32_t R = g->R, NS = g->n_slot, nm = g->E / g->R;
+  int64_t n = 0;
+  for (int32_t t = 0; t < R; t++)
+    for (int32_t s = 0; s < NS; s++) {
+      int32_t e = slot_expert[(int64_t)t * NS + s];
+      if (e >= 0 && home(g, e) == rank) n++;
+    }
+  *n_out = n;
+  if (n > cap) return ORC_ENOSPC;
+  if (n > 0 && !rgrad) return ORC_EINVAL;
+  n = 0;
+  for (int32_t t = 0; t < R; t++)
+    for (int32_t s = 0; s < NS; s++) {
+      int32_t e = slot_expert[(int64_t)t * NS + s];
+      if (e < 0 || home(g, e) != rank) continue;
+      float *mg = main_grad + (int64_t)(e - rank * nm) * W;
+      float *rg = rgrad + n * W;
+      for (int64_t i = 0; i < W; i++) {
+        volatile float sum = mg[i] + rg[i];
+        mg[i] = sum;
+        rg[i] = 0.0f;
+      }
       n++;
     }
   return ORC_OK;

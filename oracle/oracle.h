@@ -9,7 +9,8 @@
  * library; the buffer layouts below are restated here on purpose so that the
  * two sides can be compared byte for byte.
  *
- * Arithmetic: int64 everywhere, no floating point.
+ * Arithmetic: int64 everywhere; fp32 with a fixed order in the combine
+ * gather and the gradient reduction only.
  *
  * Layouts (all row-major, caller-owned host memory):
  *   R ranks, E logical experts, n_main = E / R main experts per rank,
@@ -99,6 +100,20 @@ int orc_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W,
                    int32_t rank, const orc_group *g, const int32_t *slot_expert,
                    const int32_t *slot_src, uint16_t *staging, int64_t cap,
                    int64_t *dest_off, int64_t *n_out);
+
+/* Combine gather: out[t] = bf16(sum_k fp32(gate[t][k] * y[row_of_slot[t][k]]))
+ * accumulated in fp32 in k order from +0 (no fused multiply-add); rows -1
+ * skipped.  y [n_rows][H] bf16, gate [T][k] fp32, out [T][H] bf16. */
+int orc_combine(const uint16_t *y, const float *gate, const int32_t *row_of_slot,
+                int64_t T, int32_t k, int32_t H, int64_t n_rows, uint16_t *out);
+
+/* Gradient reduction of this rank's replicated main experts: main_grad
+ * [n_main][W] fp32 += the rgrad entries [n_out][W] fp32 of each expert, in
+ * staging order (destination rank, then slot), sequentially in fp32; rgrad
+ * entries are then zeroed. */
+int orc_grad_reduce(float *main_grad, float *rgrad, int64_t W, int32_t rank,
+                    const orc_group *g, const int32_t *slot_expert, int64_t cap,
+                    int64_t *n_out);
 
 /* Diagnostics of a plan: out[0..5] = max rank load before, mean load (x1),
  * max rank load after, n_replicas, max |H(e)|, remote (in-flight) tokens. */

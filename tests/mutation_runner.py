@@ -11,6 +11,7 @@ import gen  # noqa: E402
 import oracle  # noqa: E402
 import test_oracle_invariants as inv  # noqa: E402
 import test_oracle_pins as pins  # noqa: E402
+import test_oracle_combine_reduce as cr  # noqa: E402
 import test_oracle_relay as relay  # noqa: E402
 
 
@@ -40,6 +41,17 @@ def main(lib_path, bf_exe):
         lambda: relay.test_second_hot_expert_sees_first_ones_volumes(),
         lambda: relay.test_larger_fanout_goes_first(),
         lambda: relay.test_pack_relay_stages_for_the_slots_a_rank_sends(),
+        lambda: cr.test_combine_unit_weight_k1_is_a_copy(),
+        lambda: [cr.test_combine_rounds_to_nearest_even(gt, w) for gt, w in
+                 [(1 + 2 ** -8, 0x3F80), (1 + 3 * 2 ** -8, 0x3F82), (1 + 2 ** -8 + 2 ** -20, 0x3F81)]],
+        lambda: [cr.test_combine_sums_in_fp32_in_k_order(o, w) for o, w in
+                 [((2.0 ** 25, 1.0, -2.0 ** 25), 0), ((2.0 ** 25, -2.0 ** 25, 1.0), 0x3F80)]],
+        lambda: [cr.test_combine_within_error_bound_of_the_fp64_definition(s, k) for s, k in ((0, 8), (1, 2))],
+        lambda: cr.test_grad_reduce_integer_sums_are_exact(),
+        lambda: cr.test_grad_reduce_fp32_sequential_from_the_main_value(),
+        lambda: cr.test_grad_reduce_follows_staging_order(),
+        lambda: cr.test_grad_reduce_entries_map_to_experts_in_staging_order(),
+        lambda: cr.test_grad_reduce_within_error_bound_of_the_fp64_sum(0),
     ]
     for i, chk in enumerate(checks):
         try:

@@ -61,6 +61,20 @@ MUTATIONS = {
     "relay_leaf_volume_not_counted": ("      vol[best] += 1;\n      slot_src", "      slot_src"),
     "relay_source_not_updated": ("vol[home(g, e)] -= f - n;", "vol[home(g, e)] -= 0;"),
     "pack_relay_reads_main_blob": ("src = relay_src + (int64_t)s2 * W;", "src = w_main;"),
+    "combine_k_descending": ("      for (int32_t kk = 0; kk < k; kk++) {\n        int32_t row = row_of_slot[t * k + kk];",
+                             "      for (int32_t kk = k - 1; kk >= 0; kk--) {\n        int32_t row = row_of_slot[t * k + kk];"),
+    "combine_ignores_gate": ("volatile float prod = gate[t * k + kk] * bf16_to_f32(",
+                             "volatile float prod = bf16_to_f32("),
+    "bf16_ties_away_from_zero": ("if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1;",
+                                 "if (dropped >= 0x8000u) kept += 1;"),
+    "bf16_truncates": ("if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1;",
+                       "(void)dropped;"),
+    "combine_accumulates_in_double": ("      volatile float acc = 0.0f; /* volatile",
+                                      "      volatile double acc = 0.0f; /* volatile"),
+    "grad_reduce_keeps_replicas": ("        rg[i] = 0.0f;\n", "\n"),
+    "grad_reduce_slot_major": (
+        "  n = 0;\n  for (int32_t t = 0; t < R; t++)\n    for (int32_t s = 0; s < NS; s++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e < 0 || home(g, e) != rank) continue;\n      float *mg",
+        "  n = 0;\n  for (int32_t s = 0; s < NS; s++)\n    for (int32_t t = 0; t < R; t++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e < 0 || home(g, e) != rank) continue;\n      float *mg"),
 }
 
 
@@ -98,7 +112,7 @@ def test_mutation_is_caught(bruteforce, tmp_path, name):
     (mdir / "oracle.c").write_text(src.replace(old, new))
     (mdir / "oracle.h").write_text(open(SRC[:-2] + ".h").read())
     so = str(mdir / "libmut.so")
-    subprocess.run(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-o", so,
+    subprocess.run(["gcc", "-O1", "-std=c11", "-ffp-contract=off", "-fPIC", "-shared", "-o", so,
                     str(mdir / "oracle.c")], check=True)
     # exit 3: a pin failed; a crash or a hang is also a detection
     assert _run(so, bruteforce, timeout=30) != 0, f"no pin detects {name}"
