@@ -12,6 +12,10 @@
  *                             per-destination staging
  *      ultraep_relay_plan     relay trees for hot-expert fan-out, and
  *      ultraep_pack_relay     the packing that follows them
+ *   5. ultraep_combine        reverse reroute: gate-weighted gather of the
+ *                             experts' output rows back to token order
+ *   6. ultraep_grad_reduce    local half of the gradient reduction: replica
+ *                             gradients accumulated into main gradients
  *
  * Conventions for every call:
  *   - Buffer pointers are DEVICE pointers unless marked "host".  The caller
@@ -261,6 +265,42 @@ int ultraep_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_
                        const ultraep_group *g, const ultraep_plan_buf *plan,
                        const int32_t *slot_src, uint16_t *staging, int64_t cap,
                        int64_t *dest_off, int32_t *status, hipStream_t stream);
+
+/* Reverse reroute: the combine gather (Sec. 4.2, the scatter-to-gather
+ * inversion of the token assignment).  Token t's output row is the sum of
+ * its routed slots' rows weighted by their gates:
+ *   out[t] = bf16( sum_{kk ascending, row_of_slot[t*k+kk] >= 0}
+ *                  gate[t*k+kk] * y[row_of_slot[t*k+kk]] )
+ * in fp32: every product and every partial sum rounded to fp32 (no fused
+ * multiply-add), from +0; the result rounded to bf16 to nearest-even, every
+ * NaN to 0x7FC0.  The paper fixes bf16 activations only; this order and
+ * precision are the library's reading.
+ *   y            [n_rows][H] bf16: rows in the dispatch layout (the experts'
+ *                outputs for the rows ultraep_dispatch sent)
+ *   gate         [T][k] fp32 top-k gate weights
+ *   row_of_slot  [T*k] int32 from ultraep_dispatch (-1 = not routed)
+ *   out          [T][H] bf16, fully written
+ * A row outside [-1, n_rows) raises ULTRAEP_EDATA (that slot is skipped).
+ * 1 <= k <= 64, H % 8 == 0, 16-byte aligned y and out. */
+int ultraep_combine(const uint16_t *y, int64_t n_rows, const float *gate,
+                    const int32_t *row_of_slot, int64_t T, int32_t k, int32_t H, uint16_t *out,
+                    int32_t *status, hipStream_t stream);
+
+/* Gradient reduction, local half (Sec. 4.2 backward pass, tile streaming of
+ * Sec. 6.1): every replica of a main expert of `rank` returns an fp32
+ * gradient blob, laid out like the forward staging (one [W] entry per
+ * redundant slot (t, s) whose expert has home `rank`, destination rank
+ * ascending, then slot).  Each main gradient is updated in place to
+ *   main_grad[l] = (...(main_grad[l] + r_0) + r_1 ...) + r_{f-1}
+ * element by element in fp32, its replicas' entries taken in that staging
+ * order, and every replica entry is then zeroed for reuse by the next layer.
+ *   main_grad  [n_main][W] fp32, read and written
+ *   rgrad      [cap][W] fp32, entries 0 .. n_out-1 read and zeroed
+ * n_out > cap raises ULTRAEP_ENOSPC and changes nothing.  W % 4 == 0,
+ * 16-byte aligned buffers. */
+int ultraep_grad_reduce(float *main_grad, float *rgrad, int64_t W, int32_t rank,
+                        const ultraep_group *g, const ultraep_plan_buf *plan, int64_t cap,
+                        int32_t *status, hipStream_t stream);
 
 /* Host only.  Static description of a status code. */
 const char *ultraep_strerror(int code);

@@ -96,6 +96,8 @@ def lib():
         L.ultraep_relay_plan.argtypes = [gp, pp, i32, _P, _P, _P, _P, _P]
         L.ultraep_pack_relay.argtypes = [_P, _P, i64, i32, gp, pp, _P, _P, i64, _P,
                                          _P, _P]
+        L.ultraep_combine.argtypes = [_P, i64, _P, _P, i64, i32, i32, _P, _P, _P]
+        L.ultraep_grad_reduce.argtypes = [_P, _P, i64, i32, gp, pp, i64, _P, _P]
         L.ultraep_strerror.argtypes = [ctypes.c_int]
         L.ultraep_strerror.restype = ctypes.c_char_p
         for f in ("ultraep_plan_sizes", "ultraep_count", "ultraep_plan",
@@ -103,7 +105,7 @@ def lib():
                   "ultraep_dispatch", "ultraep_dispatch_layout",
                   "ultraep_dispatch_scatter", "ultraep_pack_replicas",
                   "ultraep_reroute_and_pack", "ultraep_relay_plan",
-                  "ultraep_pack_relay"):
+                  "ultraep_pack_relay", "ultraep_combine", "ultraep_grad_reduce"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -251,6 +253,19 @@ def ultraep_pack_relay(w_main, relay_src, W, rank, g: Group, plan: Plan, slot_sr
         _ptr(w_main), _ptr(relay_src), W, rank, ctypes.byref(g), ctypes.byref(plan.c),
         _ptr(slot_src), _ptr(staging), cap, _ptr(dest_off), _ptr(status),
         _stream(stream)), "ultraep_pack_relay")
+
+
+def ultraep_combine(y, n_rows, gate, row_of_slot, T, k, H, out, status, stream=None):
+    return _check(lib().ultraep_combine(
+        _ptr(y), n_rows, _ptr(gate), _ptr(row_of_slot), T, k, H, _ptr(out), _ptr(status),
+        _stream(stream)), "ultraep_combine")
+
+
+def ultraep_grad_reduce(main_grad, rgrad, W, rank, g: Group, plan: Plan, cap, status,
+                        stream=None):
+    return _check(lib().ultraep_grad_reduce(
+        _ptr(main_grad), _ptr(rgrad), W, rank, ctypes.byref(g), ctypes.byref(plan.c), cap,
+        _ptr(status), _stream(stream)), "ultraep_grad_reduce")
 
 
 def build():

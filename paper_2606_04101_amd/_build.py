@@ -9,11 +9,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libultraep.so")
 SOURCES = ["abi.hip", "count.hip", "plan.hip", "dispatch.hip", "pack.hip",
-           "relay.hip"]
+           "relay.hip", "combine.hip", "reduce.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # packed fp32 instructions are disabled for all device code
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# the fp32 steps round every product and sum on its own: no contraction into
+# fused multiply-adds (the other sources have no fp32 arithmetic to fuse)
+EXTRA = {"combine.hip": ["-ffp-contract=off"], "reduce.hip": ["-ffp-contract=off"]}
 
 
 def build(verbose: bool = False) -> str:
@@ -22,7 +25,7 @@ def build(verbose: bool = False) -> str:
 
     def compile_one(src):
         obj = os.path.join(out_dir, src.replace(".hip", ".o"))
-        cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")

@@ -174,6 +174,29 @@ int ultraep_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_
                                    dest_off, status, stream));
 }
 
+int ultraep_combine(const uint16_t *y, int64_t n_rows, const float *gate,
+                    const int32_t *row_of_slot, int64_t T, int32_t k, int32_t H, uint16_t *out,
+                    int32_t *status, hipStream_t stream) {
+  if (T < 0 || k < 1 || k > 64 || H < 8 || H % 8 != 0 || n_rows < 0 || !status)
+    return ULTRAEP_EINVAL;
+  if (T * static_cast<int64_t>(k) >= (int64_t(1) << 31) || n_rows >= (int64_t(1) << 31))
+    return ULTRAEP_EINVAL;
+  if (T == 0) return ULTRAEP_OK;
+  if (!gate || !row_of_slot || !out || !aligned16(out)) return ULTRAEP_EINVAL;
+  if (n_rows > 0 && (!y || !aligned16(y))) return ULTRAEP_EINVAL;
+  return rc(uep::launch_combine(y, n_rows, gate, row_of_slot, T, k, H, out, status, stream));
+}
+
+int ultraep_grad_reduce(float *main_grad, float *rgrad, int64_t W, int32_t rank,
+                        const ultraep_group *g, const ultraep_plan_buf *plan, int64_t cap,
+                        int32_t *status, hipStream_t stream) {
+  if (!group_ok(g) || !plan_ok(g, plan) || rank < 0 || rank >= g->R) return ULTRAEP_EINVAL;
+  if (W < 4 || W % 4 != 0 || cap < 0 || !status || !main_grad || !aligned16(main_grad))
+    return ULTRAEP_EINVAL;
+  if (cap > 0 && (!rgrad || !aligned16(rgrad))) return ULTRAEP_EINVAL;
+  return rc(uep::launch_grad_reduce(main_grad, rgrad, W, rank, *g, *plan, cap, status, stream));
+}
+
 const char *ultraep_strerror(int code) {
   switch (code) {
     case ULTRAEP_OK: return "ok";

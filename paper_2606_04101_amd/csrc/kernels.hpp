@@ -66,4 +66,12 @@ hipError_t launch_relay(const ultraep_group &g, const ultraep_plan_buf &plan, in
                         int32_t *slot_src, int32_t *send_vol, int64_t *stats, int32_t *status,
                         hipStream_t stream);
 
+// combine gather (reverse reroute) and the local gradient reduction
+hipError_t launch_combine(const uint16_t *y, int64_t n_rows, const float *gate,
+                          const int32_t *row_of_slot, int64_t T, int32_t k, int32_t H,
+                          uint16_t *out, int32_t *status, hipStream_t stream);
+hipError_t launch_grad_reduce(float *main_grad, float *rgrad, int64_t W, int32_t rank,
+                              const ultraep_group &g, const ultraep_plan_buf &plan, int64_t cap,
+                              int32_t *status, hipStream_t stream);
+
 }  // namespace uep
