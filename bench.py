@@ -74,6 +74,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extensions", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -339,10 +340,137 @@ def main():
         "setup_s": round(setup_s, 2),
     }
 
+    if not args.no_extensions:
+        out["extensions"] = extensions(args, dev, stream, c, g, plan, load, rank, send,
+                                       ros, boff, n_routed, w, W, fan, eager_us)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(c, tk_all, rank, x_h, w_h, cap,
                                            args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def extensions(args, dev, stream, c, g, plan, load, rank, send, ros, boff, n_routed,
+               w, W, fan, eager_us):
+    """The steps next to the balancing path, each timed with HIP events on
+    the launch stream (mean over --steps launches after warm-up):
+      combine      the gate-weighted gather of the experts' output rows back
+                   to token order, on this step's dispatch layout;
+      grad_reduce  the local gradient reduction of this rank's replicated
+                   experts (fp32 gradients, blobs of the layer's size);
+      relay_plan   the relay trees of the hot experts, on this layer's plan
+                   and on the Qwen3-235B-shaped and DeepSeek-V3 prefill plans
+                   (where experts exceed four replicas);
+      pack_relay   the local packing under those trees on the
+                   Qwen3-235B-shaped layer, for the rank that sends the most.
+    Bandwidth figures use algorithmic bytes (each source byte read once,
+    each destination byte written once) against the 8 TB/s peak."""
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2606_04101_amd as uep
+
+    T, k, H = c.T, c.k, c.H
+    V = T * k
+    reps = max(5, min(args.steps, 50))
+    res = {}
+
+    def bw(nbytes, us):
+        gbps = nbytes / (us * 1e-6) / 1e9
+        return {"us": round(us, 2), "algorithmic_bytes": int(nbytes), "GBps": round(gbps, 1),
+                "frac": round(gbps / PEAK_HBM_GBPS, 4)}
+
+    def warm(f, n=3):
+        for _ in range(n):
+            f()
+        torch.cuda.synchronize()
+
+    # ---- combine on this step's layout (send stands in for the experts'
+    # output rows: same layout and size)
+    rng = np.random.default_rng(4101)
+    z = rng.standard_normal((T, k))
+    gate = torch.from_numpy((np.exp(z) / np.exp(z).sum(1, keepdims=True)).astype(np.float32)).to(dev)
+    out_t = torch.empty((T, H), dtype=torch.int16, device=dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    f = lambda: uep.ultraep_combine(send, V, gate, ros, T, k, H, out_t, st)
+    warm(f)
+    res["combine"] = bw(2 * n_routed * H + 2 * T * H + 8 * V, eager_us([f], reps))
+
+    # ---- gradient reduction of this rank's replicated experts
+    nm = c.n_main
+    n_rep = int(sum(fan))
+    mg = torch.zeros((nm, W), dtype=torch.float32, device=dev)
+    rg = torch.zeros((max(n_rep, 1), W), dtype=torch.float32, device=dev)
+    f = lambda: uep.ultraep_grad_reduce(mg, rg, W, rank, g, plan, max(n_rep, 1), st)
+    warm(f)
+    res["grad_reduce"] = bw(int(sum(4 * W * (2 + 2 * fv) for fv in fan if fv > 0)),
+                            eager_us([f], reps))
+    res["grad_reduce"]["replicas"] = n_rep
+    del mg, rg
+
+    # ---- relay trees: latency of one call, from a graph of 20 calls
+    def relay_us(gg, pl):
+        src = torch.empty(max(gg.R * gg.n_slot, 1), dtype=torch.int32, device=dev)
+        vol = torch.empty(gg.R, dtype=torch.int32, device=dev)
+        rs = torch.empty(4, dtype=torch.int64, device=dev)
+        fn = lambda: uep.ultraep_relay_plan(gg, pl, 4, src, vol, rs, st)
+        warm(fn)
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for _ in range(20):
+                fn()
+        gr.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ts = []
+        for _ in range(5):
+            e0.record()
+            gr.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(1e3 * e0.elapsed_time(e1) / 20)
+        return float(np.median(ts)), src, vol, rs.cpu().tolist()
+
+    us, _, _, rst = relay_us(g, plan)
+    rel = {c.name: {"us": round(us, 2), "relay_experts": rst[0], "max_send_blobs": [rst[2], rst[3]]}}
+    for cid in (3, 5):
+        cc = gen.config(cid)
+        gg = uep.Group(cc.R, cc.E, cc.n_slot, cc.u_min, cc.beta_num, cc.beta_den)
+        tk = torch.from_numpy(gen.topk_all(cc, 0)).to(dev)
+        ld = torch.empty((cc.R, cc.E), dtype=torch.int32, device=dev)
+        uep.ultraep_count(tk, cc.T, cc.k, cc.E, cc.R, ld, st)
+        pl = uep.Plan(gg, dev)
+        uep.ultraep_plan(ld, gg, pl)
+        us, src, vol, rst = relay_us(gg, pl)
+        rel[cc.name] = {"us": round(us, 2), "relay_experts": rst[0],
+                        "max_send_blobs": [rst[2], rst[3]]}
+        if cid == 3:  # the packing under these trees, for the busiest sender
+            r3 = int(torch.argmax(vol).item())
+            Xh = pl.slot_expert.cpu().numpy().reshape(cc.R, cc.n_slot)
+            sh = src.cpu().numpy()[: cc.R * cc.n_slot].reshape(cc.R, cc.n_slot)
+            n_send = int(((Xh >= 0) & (sh == r3)).sum())
+            srcs = {}  # source blob -> copies
+            for t in range(cc.R):
+                for s_ in range(cc.n_slot):
+                    if Xh[t, s_] >= 0 and sh[t, s_] == r3:
+                        srcs[int(Xh[t, s_])] = srcs.get(int(Xh[t, s_]), 0) + 1
+            W3 = cc.W
+            w3 = torch.zeros((cc.n_main, W3), dtype=torch.int16, device=dev)
+            rsrc = torch.zeros((cc.n_slot, W3), dtype=torch.int16, device=dev)
+            stg = torch.empty((max(n_send, 1), W3), dtype=torch.int16, device=dev)
+            doff = torch.empty(cc.R + 1, dtype=torch.int64, device=dev)
+            fn = lambda: uep.ultraep_pack_relay(w3, rsrc, W3, r3, gg, pl, src, stg,
+                                                max(n_send, 1), doff, st)
+            warm(fn)
+            res["pack_relay"] = bw(sum(2 * W3 * (1 + n) for n in srcs.values()), eager_us([fn], reps))
+            res["pack_relay"].update({"workload": cc.name, "rank": r3, "copies": n_send,
+                                      "source_blobs": len(srcs)})
+            del w3, rsrc, stg
+        del tk, ld, pl
+    res["relay_plan"] = rel
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0, f"device status {int(st.item())}"
+    return res
 
 
 def cpu_baseline(c, tk_all, rank, x_h, w_h, cap, budget_s):
