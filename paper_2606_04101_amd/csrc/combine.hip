@@ -10,9 +10,12 @@
 // bf16 to nearest-even, every NaN to 0x7FC0.
 //
 // Bandwidth bound: each routed row is read once, each output row written
-// once.  Persistent waves walk the tokens as the scatter does; a lane owns
-// 16-byte chunks (8 bf16) of the row, and for each chunk it issues the k
-// rows' loads together before the fp32 accumulation.
+// once.  A wave takes a work unit of two 16-byte chunks (8 bf16 each) per
+// lane of one token's row, issues the k rows' loads of both chunks together
+// (16 loads in flight for k = 8), accumulates and stores.  Many short waves
+// keep the most row reads in flight: on the DeepSeek-V3-shaped layer this
+// measured 90 us against 99-121 us for persistent waves that walk whole
+// rows, and against 92-105 us for units of 1, 3 or 4 chunks per lane.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -22,8 +25,10 @@ namespace uep {
 
 constexpr int kCbThreads = 256;
 constexpr int kCbWaves = kCbThreads / kWave;
-constexpr int kCbGrid = 512;
+constexpr int kCbGrid = 65535;
 constexpr int kCbMaxK = 8;  // rows loaded together per chunk
+constexpr int kCbChunks = 2;       // 16-byte chunks per lane per step
+constexpr int kCbLaneChunks = 2;   // 16-byte chunks per lane per work unit
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
@@ -71,32 +76,48 @@ __device__ __forceinline__ void token_rows(const int32_t *row_of_slot, const flo
   }
 }
 
-// k <= kCbMaxK: the k loads of a chunk in flight together
+// k <= kCbMaxK.  Work unit: kCbLaneChunks 16-byte chunks per lane of one
+// token's row; the k rows' loads of kCbChunks chunks are in flight together.
 __global__ void __launch_bounds__(kCbThreads)
 k_combine(const v4u *__restrict__ y, int64_t n_rows, const float *__restrict__ gate,
           const int32_t *__restrict__ row_of_slot, int64_t T, int32_t k, int32_t nch,
           v4u *__restrict__ out, int32_t *status) {
   const int lane = lane_id();
+  const int nblk = (nch + kCbLaneChunks * kWave - 1) / (kCbLaneChunks * kWave);
+  const int64_t n_units = T * nblk;
   const int64_t nw = static_cast<int64_t>(gridDim.x) * kCbWaves;
-  for (int64_t t = static_cast<int64_t>(blockIdx.x) * kCbWaves + threadIdx.x / kWave; t < T;
-       t += nw) {
+  for (int64_t unit = static_cast<int64_t>(blockIdx.x) * kCbWaves + threadIdx.x / kWave;
+       unit < n_units; unit += nw) {
+    const int64_t t = unit / nblk;
+    const int b = static_cast<int>(unit - t * nblk);
     int row;
     float g;
     token_rows(row_of_slot, gate, t, k, lane, n_rows, status, row, g);
-    for (int cc = lane; cc < nch; cc += kWave) {
-      v4u v[kCbMaxK];
+    const int c_end = min(nch, (b + 1) * kCbLaneChunks * kWave);
+    for (int c0 = b * kCbLaneChunks * kWave + lane; c0 < c_end; c0 += kCbChunks * kWave) {
+      v4u v[kCbChunks][kCbMaxK];
 #pragma unroll
       for (int kk = 0; kk < kCbMaxK; ++kk) {
         const int r = kk < k ? readlane(row, kk) : -1;
-        if (r >= 0) v[kk] = __builtin_nontemporal_load(y + static_cast<int64_t>(r) * nch + cc);
-      }
-      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kk = 0; kk < kCbMaxK; ++kk) {
-        const int r = kk < k ? readlane(row, kk) : -1;
-        if (r >= 0) acc_chunk(acc, __int_as_float(readlane(__float_as_int(g), kk)), v[kk]);
+        for (int u = 0; u < kCbChunks; ++u) {
+          const int cc = c0 + u * kWave;
+          if (r >= 0 && cc < c_end)
+            v[u][kk] = __builtin_nontemporal_load(y + static_cast<int64_t>(r) * nch + cc);
+        }
       }
-      __builtin_nontemporal_store(pack_chunk(acc), out + t * nch + cc);
+#pragma unroll
+      for (int u = 0; u < kCbChunks; ++u) {
+        const int cc = c0 + u * kWave;
+        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < kCbMaxK; ++kk) {
+          const int r = kk < k ? readlane(row, kk) : -1;
+          if (r >= 0 && cc < c_end)
+            acc_chunk(acc, __int_as_float(readlane(__float_as_int(g), kk)), v[u][kk]);
+        }
+        if (cc < c_end) __builtin_nontemporal_store(pack_chunk(acc), out + t * nch + cc);
+      }
     }
   }
 }
@@ -130,7 +151,8 @@ hipError_t launch_combine(const uint16_t *y, int64_t n_rows, const float *gate,
                           const int32_t *row_of_slot, int64_t T, int32_t k, int32_t H,
                           uint16_t *out, int32_t *status, hipStream_t stream) {
   const int32_t nch = H / 8;
-  const int64_t need = (T + kCbWaves - 1) / kCbWaves;
+  const int64_t units = T * ((nch + kCbLaneChunks * kWave - 1) / (kCbLaneChunks * kWave));
+  const int64_t need = (units + kCbWaves - 1) / kCbWaves;
   const dim3 grid(static_cast<unsigned>(need < kCbGrid ? need : kCbGrid));
   const v4u *ys = reinterpret_cast<const v4u *>(y);
   v4u *os = reinterpret_cast<v4u *>(out);
