@@ -1,0 +1,148 @@
+#!/usr/bin/env python3
+"""Solver-quality sweep: the balancing metrics the paper averages in Table 3
+(result imbalance, redundant slots consumed, largest host set, in-flight
+token ratio with and without the locality pass, solving time), measured for
+this library's planner over a grid of MoE, EP and redundancy settings with
+synthetic power-law initial loads (Sec. 8.5 simulates the same kind of grid).
+
+Each setting draws R ranks x T tokens of top-k routing from the seeded
+router with a Zipf-ranked expert bias of exponent alpha (power-law expert
+popularity), counts it and plans it on the GPU, then reads the plan back:
+  imbalance before / after   max rank load / mean, before and after (U)
+  replicas                   sum_e (|H(e)| - 1): redundant slots consumed
+  max_hosts                  max_e |H(e)|
+  inflight                   share of routed tokens served off their rank
+                             (from Q, which applies the locality pass)
+  inflight_no_locality       the same share if every source split its
+                             tokens over the hosts in proportion to their
+                             quotas (no locality pass), sum over experts of
+                             1 - sum_t lambda_{t,e} u_{e,t} / lambda_e, per token
+  solve_us                   ultraep_plan device latency: one call of a graph
+                             of 20 consecutive calls
+Prints one JSON line: every setting and the averages.  Needs an MI355X."""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+GRID_MOE = ((128, 8), (256, 8))   # (E, top-k): Qwen3 / GLM and DeepSeek-V3 shapes
+GRID_R = (16, 32, 64)             # EP sizes
+GRID_NS = (1, 2, 4)               # redundant slots per rank
+GRID_ALPHA = (0.2, 0.35, 0.5)     # Zipf exponent of the router bias
+
+
+def metrics(load, U, host_ptr, host_rank, Q):
+    """Table 3 metrics of one plan (host numpy arrays: load [R][E], U [E][R],
+    host_ptr [E+1], host_rank [ncol], Q [R][ncol])."""
+    import numpy as np
+    load = np.asarray(load, np.int64)
+    U = np.asarray(U, np.int64)
+    R, E = load.shape
+    L = int(load.sum())
+    mean = L / R
+    nm = E // R
+    lam_e = load.sum(0)
+    ell = lam_e.reshape(R, nm).sum(1)
+    after = U.sum(0).max()
+    nh = np.diff(np.asarray(host_ptr, np.int64))
+    remote = 0
+    for e in range(E):
+        for j in range(host_ptr[e], host_ptr[e + 1]):
+            t = host_rank[j]
+            remote += int(Q[:, j].sum() - Q[t, j])
+    local_noloc = 0.0
+    for e in range(E):
+        if lam_e[e] == 0:
+            continue
+        for j in range(host_ptr[e], host_ptr[e + 1]):
+            t = host_rank[j]
+            local_noloc += load[t, e] * U[e, t] / lam_e[e]
+    return {
+        "imbalance_before": float(ell.max() / mean) if L else 1.0,
+        "imbalance_after": float(after / mean) if L else 1.0,
+        "replicas": int((nh - 1).sum()),
+        "sum_hosts": int(nh.sum()),
+        "max_hosts": int(nh.max()),
+        "inflight": remote / L if L else 0.0,
+        "inflight_no_locality": 1.0 - local_noloc / L if L else 0.0,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--tokens", type=int, default=8192, help="tokens per rank")
+    ap.add_argument("--quick", action="store_true", help="one skew level, R = 64 only")
+    args = ap.parse_args()
+
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2606_04101_amd as uep
+
+    dev = torch.device("cuda:0")
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    rows = []
+    t0 = time.time()
+    sid = 0
+    for E, k in GRID_MOE:
+        for R in (GRID_R if not args.quick else (64,)):
+            for NS in GRID_NS:
+                for alpha in (GRID_ALPHA if not args.quick else (0.35,)):
+                    sid += 1
+                    c = gen.Config(200 + sid, f"sweep{sid}", R=R, E=E, n_slot=NS, k=k, T=args.tokens,
+                                   H=8, F=8, u_min=1024, bias="zipf", zipf_s=1.0,
+                                   bias_scale=alpha)
+                    tk = torch.from_numpy(gen.topk_all(c, 0)).to(dev)
+                    g = uep.Group(R, E, NS, c.u_min, c.beta_num, c.beta_den)
+                    load = torch.empty((R, E), dtype=torch.int32, device=dev)
+                    uep.ultraep_count(tk, c.T, k, E, R, load, st)
+                    plan = uep.Plan(g, dev)
+                    fn = lambda: uep.ultraep_plan(load, g, plan)
+                    fn()
+                    torch.cuda.synchronize()
+                    gr = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(gr):
+                        for _ in range(20):
+                            fn()
+                    gr.replay()
+                    torch.cuda.synchronize()
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    ts = []
+                    for _ in range(5):
+                        e0.record()
+                        gr.replay()
+                        e1.record()
+                        torch.cuda.synchronize()
+                        ts.append(1e3 * e0.elapsed_time(e1) / 20)
+                    assert int(st.item()) == 0 and int(plan.stats[6].item()) == 0
+                    ncol = g.ncol
+                    m = metrics(load.cpu().numpy(), plan.quota.cpu().numpy().reshape(E, R),
+                                plan.host_ptr.cpu().numpy(), plan.host_rank.cpu().numpy(),
+                                plan.reroute.cpu().numpy().reshape(R, ncol).astype(np.int64))
+                    m.update({"E": E, "k": k, "R": R, "n_slot": NS, "alpha": alpha,
+                              "tau_star": int(plan.stats[0].item()),
+                              "probes": int(plan.stats[3].item()),
+                              "solve_us": round(float(np.median(ts)), 2)})
+                    rows.append(m)
+                    print(f"# E={E} R={R} n_slot={NS} alpha={alpha}: before {m['imbalance_before']:.2f} "
+                          f"after {m['imbalance_after']:.3f} replicas {m['replicas']} max|H| {m['max_hosts']} "
+                          f"inflight {m['inflight']:.3f}/{m['inflight_no_locality']:.3f} "
+                          f"solve {m['solve_us']} us", file=sys.stderr, flush=True)
+                    del gr, plan, load, tk
+    keys = ("imbalance_before", "imbalance_after", "replicas", "sum_hosts", "max_hosts", "inflight",
+            "inflight_no_locality", "solve_us")
+    avg = {kk: round(float(np.mean([r[kk] for r in rows])), 4) for kk in keys}
+    print(json.dumps({"metric": "solver quality over a grid of synthetic power-law loads (Table 3 metrics)",
+                      "settings": len(rows), "tokens_per_rank": args.tokens, "average": avg,
+                      "elapsed_s": round(time.time() - t0, 1), "rows": rows}), flush=True)
+
+
+if __name__ == "__main__":
+    main()
