@@ -76,7 +76,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extensions", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--workloads", action="store_true",
+                    help="instead of the step: count, plan, dispatch and pack of every "
+                         "workload, with the oracle beside them (one JSON line each)")
     args = ap.parse_args()
+    if args.workloads:
+        return per_workload(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the "
               "balancing path is replicated per rank and its collectives are not "
@@ -471,6 +476,140 @@ def extensions(args, dev, stream, c, g, plan, load, rank, send, ros, boff, n_rou
     torch.cuda.synchronize()
     assert int(st.item()) == 0, f"device status {int(st.item())}"
     return res
+
+
+def per_workload(args):
+    """Count, plan, dispatch and pack of each of the five workloads on its
+    measured rank (most outbound replicas), each event-timed (mean over up
+    to 50 launches after warm-up), the oracle timed once beside it on the
+    same inputs, and the outputs compared byte for byte."""
+    import numpy as np
+    import torch
+
+    import gen
+    import oracle
+    import paper_2606_04101_amd as uep
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    reps = max(5, min(args.steps, 50))
+
+    def ev_us(fns, n=reps):
+        for f in fns:
+            f()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        torch.cuda.synchronize()
+        e[0].record(stream)
+        for i in range(n):
+            for f in fns:
+                f()
+            e[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return 1e3 * float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(n)]))
+
+    def graph_us(fns, n=20):
+        for f in fns:
+            f()
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for _ in range(n):
+                for f in fns:
+                    f()
+        gr.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ts = []
+        for _ in range(5):
+            e0.record()
+            gr.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(1e3 * e0.elapsed_time(e1) / n)
+        return float(np.median(ts))
+
+    def wall_us(f):
+        t0 = time.perf_counter()
+        r = f()
+        return r, 1e6 * (time.perf_counter() - t0)
+
+    for cid in sorted(gen.CONFIGS):
+        c = gen.config(cid)
+        g = uep.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+        og = oracle.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+        T, k, H, W = c.T, c.k, c.H, c.W
+        V = T * k
+        tk_all = gen.topk_all(c, 0)
+        tk_d = torch.from_numpy(tk_all).to(dev)
+        st = torch.zeros(1, dtype=torch.int32, device=dev)
+        load = torch.empty((c.R, c.E), dtype=torch.int32, device=dev)
+        uep.ultraep_count(tk_d, T, k, c.E, c.R, load, st)
+        plan = uep.Plan(g, dev)
+        uep.ultraep_plan(load, g, plan)
+        torch.cuda.synchronize()
+        X = plan.slot_expert.cpu().numpy().reshape(c.R, c.n_slot)
+        outb = [int(((X >= 0) & (X // c.n_main == r)).sum()) for r in range(c.R)]
+        rank = int(np.argmax(outb))
+        tk_r = tk_d[rank].contiguous()
+        load_r = load[rank]
+        x_h = gen.activations(c, 0, rank)
+        w_h = gen.weights(c, rank)
+        x = torch.from_numpy(x_h.view(np.int16)).to(dev)
+        w = torch.from_numpy(w_h.view(np.int16)).to(dev)
+        send = torch.empty((V, H), dtype=torch.int16, device=dev)
+        ros = torch.empty(V, dtype=torch.int32, device=dev)
+        boff = torch.empty(c.R * g.S + 1, dtype=torch.int64, device=dev)
+        ws = torch.empty(uep.ultraep_dispatch_ws_bytes(T, k, g), dtype=torch.uint8, device=dev)
+        cap = max(1, outb[rank])
+        stg = torch.empty((cap, W), dtype=torch.int16, device=dev)
+        doff = torch.empty(c.R + 1, dtype=torch.int64, device=dev)
+        count_f = lambda: uep.ultraep_count(tk_r, T, k, c.E, 1, load_r, st)
+        plan_f = lambda: uep.ultraep_plan(load, g, plan)
+        disp_f = lambda: uep.ultraep_dispatch(x, tk_r, T, k, H, rank, g, plan, send, ros, boff,
+                                              ws, st)
+        scat_f = lambda: uep.ultraep_dispatch_scatter(x, T, k, H, ros, boff[-1:], send)
+        pack_f = lambda: uep.ultraep_pack_replicas(w, W, rank, g, plan, stg, cap, doff, st)
+        rec = {"workload": c.name, "R": c.R, "E": c.E, "n_slot": c.n_slot, "k": k, "T": T,
+               "H": H, "F": c.F, "rank": rank, "replicas_shipped": outb[rank]}
+        rec["count_us"] = round(graph_us([count_f]), 2)
+        rec["plan_us"] = round(graph_us([plan_f]), 2)
+        rec["count_plan_us"] = round(graph_us([count_f, plan_f]), 2)
+        rec["replicate_us"] = round(graph_us([lambda: uep.ultraep_plan_replicate(load, g, plan)]), 2)
+        rec["reroute_us"] = round(graph_us([lambda: uep.ultraep_plan_reroute(load, g, plan)]), 2)
+        rec["max_hosts"] = int(plan.stats[5].item())
+        rec["dispatch_us"] = round(ev_us([disp_f]), 2)
+        rec["scatter_us"] = round(ev_us([scat_f]), 2)
+        rec["pack_us"] = round(ev_us([pack_f]), 2) if outb[rank] else 0.0
+        torch.cuda.synchronize()
+        assert int(st.item()) == 0, int(st.item())
+        n_routed = int(boff[-1].item())
+        sb = 2 * T * H + 2 * n_routed * H + 4 * V
+        fan = np.bincount(X[(X >= 0) & (X // c.n_main == rank)] - rank * c.n_main,
+                          minlength=c.n_main)
+        pb = int(sum(2 * W * (1 + f) for f in fan if f > 0))
+        rec["scatter_bytes"] = sb
+        rec["scatter_GBps"] = round(sb / rec["scatter_us"] / 1e3, 1)
+        rec["pack_bytes"] = pb
+        rec["pack_GBps"] = round(pb / rec["pack_us"] / 1e3, 1) if pb else None
+        # the oracle, single-threaded, once each, on the same inputs
+        (ocnt, _), t_cnt = wall_us(lambda: oracle.count(tk_all, c.E, c.R))
+        op, t_plan = wall_us(lambda: oracle.plan(ocnt, og))
+        (osend, oros, oboff, _), t_disp = wall_us(lambda: oracle.dispatch(x_h, tk_all[rank], rank, og, op))
+        (ostg, odoff, n_out, _), t_pack = wall_us(lambda: oracle.pack(w_h, rank, og, op, cap))
+        exact = (np.array_equal(load.cpu().numpy(), ocnt)
+                 and all(np.array_equal(getattr(plan, f).cpu().numpy().reshape(-1),
+                                        getattr(op, f).reshape(-1)) for f in uep.PLAN_FIELDS)
+                 and np.array_equal(ros.cpu().numpy(), oros)
+                 and np.array_equal(boff.cpu().numpy(), oboff)
+                 and np.array_equal(send.cpu().numpy().view(np.uint16), osend)
+                 and np.array_equal(doff.cpu().numpy(), odoff)
+                 and np.array_equal(stg[:n_out].cpu().numpy().view(np.uint16), ostg[:n_out]))
+        rec["oracle_us"] = {"count_all_ranks": round(t_cnt, 1), "count_one_rank": round(t_cnt / c.R, 1),
+                            "plan": round(t_plan, 1), "dispatch": round(t_disp, 1),
+                            "pack": round(t_pack, 1), "cores": 1}
+        rec["bit_exact"] = bool(exact)
+        print(json.dumps(rec), flush=True)
+        del x, w, send, stg, tk_d, plan, load
 
 
 def cpu_baseline(c, tk_all, rank, x_h, w_h, cap, budget_s):

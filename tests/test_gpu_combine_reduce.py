@@ -226,3 +226,83 @@ def test_grad_reduce_capacity():
     torch.cuda.synchronize()
     assert int(st.item()) == uep.ULTRAEP_ENOSPC
     assert (mg.cpu().numpy() == 1).all() and (rg.cpu().numpy() == 1).all()
+
+
+def test_graph_replay_of_relay_combine_reduce():
+    """ultraep_relay_plan, ultraep_pack_relay, ultraep_combine and
+    ultraep_grad_reduce captured in one HIP graph after count, plan and
+    dispatch, replayed several times with the outputs poisoned and the
+    gradient inputs restored between replays; every replay equals the eager
+    result."""
+    c = gen.config(3)
+    g, og = gp.groups(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+    tk_all = gen.topk_all(c, 0)
+    load0, _ = oracle.count(tk_all, c.E, c.R)
+    op = oracle.plan(load0, og)
+    X = op.slot_expert
+    r = int(np.argmax([((X >= 0) & (X // c.n_main == q)).sum() for q in range(c.R)]))
+    T, k, H = 512, c.k, 256          # combine over 512 tokens of narrow rows
+    W = 8 * 256
+    rng = np.random.default_rng(21)
+    dev = gp.DEV
+    tk_all_d = gp.dev_i32(tk_all)
+    load = torch.empty((c.R, c.E), dtype=torch.int32, device=dev)
+    st = gp.zero_status()
+    plan = uep.Plan(g, dev)
+    V = T * k
+    send = torch.empty((V, H), dtype=torch.int16, device=dev)
+    ros = torch.empty(V, dtype=torch.int32, device=dev)
+    gate = torch.from_numpy(softmax_gates(rng, T, k)).to(dev)
+    out = torch.empty((T, H), dtype=torch.int16, device=dev)
+    src = torch.empty(c.R * c.n_slot, dtype=torch.int32, device=dev)
+    vol = torch.empty(c.R, dtype=torch.int32, device=dev)
+    rst = torch.empty(4, dtype=torch.int64, device=dev)
+    cap = c.R * c.n_slot
+    w = gp.dev_u16(rng.integers(0, 1 << 16, (c.n_main, W), dtype=np.uint16))
+    rsrc = gp.dev_u16(rng.integers(0, 1 << 16, (c.n_slot, W), dtype=np.uint16))
+    stg = torch.zeros((cap, W), dtype=torch.int16, device=dev)
+    doff = torch.empty(c.R + 1, dtype=torch.int64, device=dev)
+    mg0 = torch.from_numpy(rng.standard_normal((c.n_main, 64)).astype(np.float32)).to(dev)
+    rg0 = torch.from_numpy(rng.standard_normal((cap, 64)).astype(np.float32)).to(dev)
+    mg, rg = mg0.clone(), rg0.clone()
+
+    def step():
+        uep.ultraep_count(tk_all_d, c.T, k, c.E, c.R, load, st)
+        uep.ultraep_plan(load, g, plan)
+        uep.ultraep_relay_plan(g, plan, 1, src, vol, rst, st)
+        uep.ultraep_pack_relay(w, rsrc, W, r, g, plan, src, stg, cap, doff, st)
+        uep.ultraep_grad_reduce(mg, rg, 64, r, g, plan, cap, st)
+        uep.ultraep_combine(send, V, gate, ros, T, k, H, out, st)
+
+    # a fixed layout for the combine: rows in slot order, every 7th masked
+    ros.copy_(torch.arange(V, dtype=torch.int32, device=dev))
+    ros[::7] = -1
+    send.copy_(torch.from_numpy(bf16_normals(rng, (V, H)).view(np.int16)).to(dev))
+    outs = lambda: [t.clone() for t in (load, src, vol, rst, stg, doff, mg, rg, out,
+                                        *[getattr(plan, f) for f in uep.PLAN_FIELDS])]
+    step()
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    ref = outs()
+    mg.copy_(mg0)
+    rg.copy_(rg0)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for i in range(4):
+        for t in (load, src, vol, rst, doff, out, *[getattr(plan, f) for f in uep.PLAN_FIELDS]):
+            t.fill_(-1)
+        mg.copy_(mg0)
+        rg.copy_(rg0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs(), ref):
+            assert torch.equal(a, b), f"replay {i} differs"
+        assert int(st.item()) == 0

@@ -265,3 +265,15 @@ def test_bruteforce_small_random_groups(orc, bruteforce):
         opt = _bf(bruteforce, R, g.E, NS, lam)
         after = p.quota.sum(0).max()
         assert opt <= after <= p.tau_star
+
+
+def test_expert_blob_size_matches_the_papers_slot_figure():
+    """Sec. 4.1: one redundant slot of Qwen3-235B-A22B holds 36 MB of bf16
+    weights per layer (gate, up and down of H = 4096, F = 1536), 3.3 GB over
+    its 94 MoE layers; the blob of the Qwen3-shaped workload is exactly
+    that."""
+    import gen
+    c = gen.config(3)
+    nbytes = 2 * c.W
+    assert nbytes == 3 * 4096 * 1536 * 2 == 36 * 2 ** 20
+    assert abs(94 * nbytes / 2 ** 30 - 3.3) < 0.05
