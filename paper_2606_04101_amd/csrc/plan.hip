@@ -742,8 +742,10 @@ __device__ __forceinline__ void reroute_small(int h, uint64_t rep, int lamhat_r,
 // Any number of hosts: lane i is host i (home first, then replicas by
 // ascending rank) with residual quota ures; the sources run in ascending
 // order, each splitting its residual demand by largest remainder.  Writes
-// q of source r, host `lane` to qcol[r * ncol].
-template <bool kExact, bool kOneRow>
+// q of source r, host `lane` to qcol[r * ncol].  kNH > 0: exactly kNH
+// hosts, the remainder ranking unrolled over lanes 0 .. kNH-1 with no
+// branch.
+template <bool kExact, bool kOneRow, int kNH>
 __device__ __forceinline__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int R,
                            int64_t ncol, int32_t *qcol, int t_i, int qloc_i) {
   const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
@@ -775,9 +777,17 @@ __device__ __forceinline__ void split_many(int lane, int nh, int lamhat_r, int D
       const int left = lh - (kOneRow ? readlane(row_sum(b), 0) : wave_sum(b));
       // the `left` hosts with the largest remainders (ties: earlier host)
       int rk = 0;
-      for (int j = 0; j < nh; ++j) {
-        const int rj = readlane(rem, j);
-        rk += (rj > rem) || (rj == rem && j < lane);
+      if (kNH > 0) {
+#pragma unroll
+        for (int j = 0; j < kNH; ++j) {
+          const int rj = readlane(rem, j);
+          rk += (rj > rem) || (rj == rem && j < lane);
+        }
+      } else {
+        for (int j = 0; j < nh; ++j) {
+          const int rj = readlane(rem, j);
+          rk += (rj > rem) || (rj == rem && j < lane);
+        }
       }
       qi = b + ((host && rk < left) ? 1 : 0);
       ures -= qi;
@@ -844,14 +854,22 @@ __device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0,
     const int qloc_i = __shfl(loc_r, t_i);
     const int ures_i = lane < nh ? ures_t : 0;
     int32_t *qcol = a.q + j0 + lane;
-    if (exact && nh <= 16)
-      split_many<true, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    if (exact && nh == 5)
+      split_many<true, true, 5>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (exact && nh == 6)
+      split_many<true, true, 6>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (exact && nh == 7)
+      split_many<true, true, 7>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (exact && nh == 8)
+      split_many<true, true, 8>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    else if (exact && nh <= 16)
+      split_many<true, true, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
     else if (exact)
-      split_many<true, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+      split_many<true, false, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
     else if (nh <= 16)
-      split_many<false, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+      split_many<false, true, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
     else
-      split_many<false, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+      split_many<false, false, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
   }
   // CSR padding columns of Q
   for (int j = total + e; j < ncol; j += E)
