@@ -729,8 +729,9 @@ int orc_pack_relay(const uint16_t *w_main, const uint16_t *relay_src, int64_t W,
 /* bf16 <-> fp32.  A bf16 pattern is the upper half of an fp32 pattern, so
  * widening is exact.  Narrowing rounds to nearest, ties to even: keep the
  * upper 16 bits, and add one unit of the kept part when the dropped 16 bits
- * exceed half a unit, or equal half a unit with an odd kept part.  NaNs
- * become the quiet NaN 0x7FC0 (sign kept). */
+ * exceed half a unit, or equal half a unit with an odd kept part.  Every
+ * NaN becomes the quiet NaN 0x7FC0 (the sign of a NaN that an invalid
+ * operation produces differs between processors). */
 static float bf16_to_f32(uint16_t b) {
   uint32_t u = (uint32_t)b << 16;
   float f;
@@ -741,8 +742,8 @@ static float bf16_to_f32(uint16_t b) {
 static uint16_t f32_to_bf16(float f) {
   uint32_t u;
   memcpy(&u, &f, 4);
-  uint32_t sign = u & 0x80000000u, mag = u & 0x7FFFFFFFu;
-  if (mag > 0x7F800000u) return (uint16_t)((sign >> 16) | 0x7FC0u); /* NaN */
+  uint32_t mag = u & 0x7FFFFFFFu;
+  if (mag > 0x7F800000u) return (uint16_t)0x7FC0u; /* NaN */
   uint32_t kept = u >> 16, dropped = u & 0xFFFFu;
   if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1; /* may carry into the exponent: correct, up to inf */
   return (uint16_t)kept;
