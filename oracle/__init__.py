@@ -88,12 +88,10 @@ def _load(path):
     L.orc_relay.argtypes = [gp, _P, _P, _P, _P, i32, _P, _P, _P]
     L.orc_pack_relay.argtypes = [_P, _P, i64, i32, gp, _P, _P, _P, i64, _P, _P]
     L.orc_combine.argtypes = [_P, _P, _P, i64, i32, i32, i64, _P]
-    L.orc_ordinals.argtypes = [_P, i64, i32, i32, _P, _P]
     L.orc_grad_reduce.argtypes = [_P, _P, i64, i32, gp, _P, i64, _P]
     for f in ("orc_count", "orc_probe", "orc_plan", "orc_bisect_trace",
               "orc_apportion", "orc_dispatch", "orc_pack", "orc_metrics",
-              "orc_relay", "orc_pack_relay", "orc_combine", "orc_grad_reduce",
-              "orc_ordinals"):
+              "orc_relay", "orc_pack_relay", "orc_combine", "orc_grad_reduce"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -133,17 +131,6 @@ def count(topk, E, n_groups=1):
     counts = np.zeros((n_groups, E), np.int32)
     st = lib().orc_count(_p(topk), T, k, E, n_groups, _p(counts))
     return counts, st
-
-
-def ordinals(topk, E):
-    """-> (ordinals [T*k] int32, counts [E] int32, status) of one block of
-    routing ids [T, k]."""
-    topk = _c(topk, np.int32)
-    T, k = topk.shape
-    ords = np.zeros(T * k, np.int32)
-    counts = np.zeros(E, np.int32)
-    st = lib().orc_ordinals(_p(topk), T, k, E, _p(ords), _p(counts))
-    return ords, counts, st
 
 
 def probe(load, g: Group, tau):

@@ -431,29 +431,6 @@ int orc_plan(const int32_t *load, const orc_group *g, int32_t locality,
   return lemma_st;
 }
 
-/* Slot ordinals (Sec. 5.2 Token Assignment): the ordinal of a routed slot
- * i = t * k + kk is the number of earlier slots (in flat token-major order)
- * routed to the same expert; masked slots (-1) get -1.  counts[e] is the
- * number of slots routed to e. */
-int orc_ordinals(const int32_t *topk, int64_t T, int32_t k, int32_t E, int32_t *ordinals,
-                 int32_t *counts) {
-  if (T < 0 || k < 1 || E < 1 || !counts || (T * k > 0 && (!topk || !ordinals)))
-    return ORC_EINVAL;
-  int status = ORC_OK;
-  for (int32_t e = 0; e < E; e++) counts[e] = 0;
-  for (int64_t i = 0; i < T * k; i++) {
-    int32_t e = topk[i];
-    if (e >= 0 && e < E) {
-      ordinals[i] = counts[e];
-      counts[e] += 1;
-    } else {
-      ordinals[i] = -1;
-      if (e != -1) status = ORC_EDATA;
-    }
-  }
-  return status;
-}
-
 /* ------------------------------------------------------------------ */
 /* Step 3 — token assignment and dispatch layout (Sec. 5.2)           */
 /* ------------------------------------------------------------------ */

@@ -69,11 +69,6 @@ int orc_bisect_trace(const int32_t *load, const orc_group *g, int64_t *taus,
 int orc_apportion(int64_t demand, const int64_t *ures, int32_t nh,
                   int64_t *out);
 
-/* Ordinal of every routed slot among the earlier slots of its expert
- * (token-major order), -1 for masked slots; counts[E] per expert. */
-int orc_ordinals(const int32_t *topk, int64_t T, int32_t k, int32_t E, int32_t *ordinals,
-                 int32_t *counts);
-
 /* Dispatch for one source rank: per-slot destination rows, block offsets and
  * the bf16 row scatter (bit copy of H uint16 per row). */
 int orc_dispatch(const uint16_t *x, const int32_t *topk, int64_t T, int32_t k,

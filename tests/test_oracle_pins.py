@@ -277,28 +277,3 @@ def test_expert_blob_size_matches_the_papers_slot_figure():
     nbytes = 2 * c.W
     assert nbytes == 3 * 4096 * 1536 * 2 == 36 * 2 ** 20
     assert abs(94 * nbytes / 2 ** 30 - 3.3) < 0.05
-
-
-@pytest.mark.parametrize("seed", [0, 1, 2])
-def test_ordinals_are_a_stable_counting_sort(orc, seed):
-    """Slot ordinals: sorting the routed slots by (expert, ordinal) is the
-    stable sort of the slots by expert (numpy's stable argsort), ordinals
-    run 0 .. count-1 per expert, masked slots get -1."""
-    rng = np.random.default_rng(seed)
-    E, T, k = 24, 300, 3
-    tk = rng.integers(0, E, (T, k)).astype(np.int32)
-    tk[rng.random((T, k)) < 0.2] = -1
-    ords, counts, st = orc.ordinals(tk, E)
-    assert st == orc.OK
-    flat = tk.reshape(-1)
-    valid = np.nonzero(flat >= 0)[0]
-    assert (ords[flat < 0] == -1).all()
-    stable = valid[np.argsort(flat[valid], kind="stable")]
-    by_key = valid[np.lexsort((ords[valid], flat[valid]))]
-    assert np.array_equal(stable, by_key)
-    assert np.array_equal(counts, np.bincount(flat[valid], minlength=E))
-    for e in range(E):
-        assert sorted(ords[flat == e].tolist()) == list(range(counts[e]))
-    bad = tk.copy()
-    bad[0, 0] = E
-    assert orc.ordinals(bad, E)[2] == orc.EDATA
