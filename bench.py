@@ -21,8 +21,10 @@ steps launched one graph per step.  (Running the packing on a
 second stream instead measured slower on one GPU: the cross-queue
 dependencies of the graph cost more than the overlap gains.)  The graph's outputs are checked
 against an eager step.  A second pass of K eager steps records a HIP event
-between consecutive launches on the launch stream; the dominant kernel's
-average duration gives the roofline figures, and count + plan is timed as
+between consecutive launches on the launch stream (the stream holds on a
+short spin kernel while the host enqueues the pass, so the events bracket
+back-to-back kernels, not host gaps); the dominant kernel's average
+duration gives the roofline figures, and count + plan is timed as
 one pair (count_plan_eager_us).  count_plan_us is the same pair's device
 latency: 20 consecutive pairs in one graph, replayed, divided by 20.  The CPU oracle is timed
 single-threaded on a bounded sample of the same workload.
@@ -45,6 +47,13 @@ METRIC = ("plan+dispatch latency per layer-microbatch (µs); "
           "dispatch/pack HBM GB/s vs peak")
 PEAK_HBM_GBPS = 8000.0
 WORKLOAD_ID = 4
+
+
+def hold_stream(ms=40.0):
+    """Keeps the current stream busy for about `ms` milliseconds (a spin
+    kernel) so that the host can enqueue a timed sequence ahead of the GPU."""
+    import torch
+    torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
 
 
 def kernel_source_digest(files):
@@ -199,19 +208,22 @@ def main():
     del graph1
 
     # ---------------- eager pass with a HIP event between consecutive launches
-    # on the launch stream: call i lasts from event i to event i + 1
+    # on the launch stream: call i lasts from event i to event i + 1.  The
+    # stream first holds on a short spin while the host enqueues the whole
+    # pass, so no launch waits on the host and an event pair brackets the
+    # kernel alone (plus the event itself)
     stream = torch.cuda.current_stream()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
            for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t_start = time.perf_counter()
+    hold_stream()
     for i in range(args.steps):
         evs[i][0].record(stream)
         for j, (_, f) in enumerate(calls):
             f()
             evs[i][j + 1].record(stream)
     torch.cuda.synchronize()
-    t_eager = (time.perf_counter() - t_start) / args.steps
+    t_eager = 1e-3 * evs[0][0].elapsed_time(evs[-1][-1]) / args.steps
 
     def span_us(j0, j1):
         return 1e3 * float(np.mean([evs[i][j0].elapsed_time(evs[i][j1])
@@ -225,6 +237,7 @@ def main():
     def eager_us(fns, reps):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
         torch.cuda.synchronize()
+        hold_stream()
         e[0].record(stream)
         for i in range(reps):
             for f in fns:
