@@ -189,11 +189,18 @@ def main():
     torch.cuda.synchronize()
     for a, b in zip(outputs, ref):
         assert torch.equal(a, b), "graph replay differs from the eager step"
+    # a HIP event between consecutive replays gives the spread of the step
+    # time (per replay) next to the wall-clock mean
+    n_rep = args.steps // G
+    rep_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_rep + 1)]
     t_start = time.perf_counter()
-    for _ in range(args.steps // G):
+    rep_ev[0].record()
+    for i in range(n_rep):
         graph.replay()
+        rep_ev[i + 1].record()
     torch.cuda.synchronize()
     t_graph = (time.perf_counter() - t_start) / args.steps
+    rep_us = [1e3 * rep_ev[i].elapsed_time(rep_ev[i + 1]) / G for i in range(n_rep)]
     del ref, graph
     # the same steps with one step per graph launch, for reference
     graph1 = make_graph(1)
@@ -316,6 +323,10 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(t_graph * 1e3, 4),
+        "step_us_spread": {"per": f"graph replay of {G} steps", "replays": n_rep,
+                           "p10": round(float(np.percentile(rep_us, 10)), 2),
+                           "median": round(float(np.median(rep_us)), 2),
+                           "p90": round(float(np.percentile(rep_us, 90)), 2)},
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -492,10 +503,23 @@ def extensions(args, dev, stream, c, g, plan, load, rank, send, ros, boff, n_rou
 
 
 def per_workload(args):
-    """Count, plan, dispatch and pack of each of the five workloads on its
-    measured rank (most outbound replicas), each event-timed (mean over up
-    to 50 launches after warm-up), the oracle timed once beside it on the
-    same inputs, and the outputs compared byte for byte."""
+    """Count, plan, dispatch and pack of the five workloads, each on its
+    measured rank (most outbound replicas), the oracle run beside it on the
+    same inputs and every output compared byte for byte.  The Qwen3-235B-
+    shaped workload runs all 16 microbatches of its drifting router and the
+    DeepSeek-V3 prefill workload all 58 layers (each reported, then the
+    median; the prefill layers' count + plan also back to back in one graph).
+    Timing:
+      count, plan, replicate, reroute   graph of 20 consecutive calls, replayed
+                                        5 times: median per call
+      dispatch, scatter, pack           one HIP event pair per launch (the
+                                        stream holds while the host enqueues),
+                                        50 launches (20 for the prefill
+                                        layers), each after an untimed 512 MiB
+                                        write that evicts the 256 MB MALL:
+                                        median, p10, p90
+    Every layer and microbatch uses the activations and weights of the first
+    one's measured rank (the bytes moved do not depend on their values)."""
     import numpy as np
     import torch
 
@@ -505,20 +529,26 @@ def per_workload(args):
 
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    reps = max(5, min(args.steps, 50))
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
 
-    def ev_us(fns, n=reps):
-        for f in fns:
+    def pct(ts):
+        ts = np.asarray(ts)
+        return {"median": round(float(np.median(ts)), 2), "p10": round(float(np.percentile(ts, 10)), 2),
+                "p90": round(float(np.percentile(ts, 90)), 2)}
+
+    def cold_us(f, n):
+        f()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n)]
+        hold_stream()
+        for e0, e1 in ev:
+            scratch.zero_()
+            e0.record(stream)
             f()
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+            e1.record(stream)
         torch.cuda.synchronize()
-        e[0].record(stream)
-        for i in range(n):
-            for f in fns:
-                f()
-            e[i + 1].record(stream)
-        torch.cuda.synchronize()
-        return 1e3 * float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(n)]))
+        return pct([1e3 * e0.elapsed_time(e1) for e0, e1 in ev])
 
     def graph_us(fns, n=20):
         for f in fns:
@@ -539,20 +569,19 @@ def per_workload(args):
             e1.record()
             torch.cuda.synchronize()
             ts.append(1e3 * e0.elapsed_time(e1) / n)
-        return float(np.median(ts))
+        return round(float(np.median(ts)), 2)
 
     def wall_us(f):
         t0 = time.perf_counter()
         r = f()
-        return r, 1e6 * (time.perf_counter() - t0)
+        return r, round(1e6 * (time.perf_counter() - t0), 1)
 
-    for cid in sorted(gen.CONFIGS):
-        c = gen.config(cid)
-        g = uep.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
-        og = oracle.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+    def instance(c, m, g, og, xw, n_cold):
+        """One microbatch / layer m of workload c; xw holds the activations and
+        weights (host and device) of the first instance's measured rank."""
         T, k, H, W = c.T, c.k, c.H, c.W
         V = T * k
-        tk_all = gen.topk_all(c, 0)
+        tk_all = gen.topk_all(c, m)
         tk_d = torch.from_numpy(tk_all).to(dev)
         st = torch.zeros(1, dtype=torch.int32, device=dev)
         load = torch.empty((c.R, c.E), dtype=torch.int32, device=dev)
@@ -563,18 +592,19 @@ def per_workload(args):
         X = plan.slot_expert.cpu().numpy().reshape(c.R, c.n_slot)
         outb = [int(((X >= 0) & (X // c.n_main == r)).sum()) for r in range(c.R)]
         rank = int(np.argmax(outb))
+        if not xw:
+            x_h, w_h = gen.activations(c, m, rank), gen.weights(c, rank)
+            xw.update(x_h=x_h, w_h=w_h, x=torch.from_numpy(x_h.view(np.int16)).to(dev),
+                      w=torch.from_numpy(w_h.view(np.int16)).to(dev),
+                      send=torch.empty((V, H), dtype=torch.int16, device=dev),
+                      stg=torch.empty((max(1, c.R * c.n_slot), W), dtype=torch.int16, device=dev))
+        x, w, send, stg = xw["x"], xw["w"], xw["send"], xw["stg"]
         tk_r = tk_d[rank].contiguous()
         load_r = load[rank]
-        x_h = gen.activations(c, 0, rank)
-        w_h = gen.weights(c, rank)
-        x = torch.from_numpy(x_h.view(np.int16)).to(dev)
-        w = torch.from_numpy(w_h.view(np.int16)).to(dev)
-        send = torch.empty((V, H), dtype=torch.int16, device=dev)
         ros = torch.empty(V, dtype=torch.int32, device=dev)
         boff = torch.empty(c.R * g.S + 1, dtype=torch.int64, device=dev)
         ws = torch.empty(uep.ultraep_dispatch_ws_bytes(T, k, g), dtype=torch.uint8, device=dev)
         cap = max(1, outb[rank])
-        stg = torch.empty((cap, W), dtype=torch.int16, device=dev)
         doff = torch.empty(c.R + 1, dtype=torch.int64, device=dev)
         count_f = lambda: uep.ultraep_count(tk_r, T, k, c.E, 1, load_r, st)
         plan_f = lambda: uep.ultraep_plan(load, g, plan)
@@ -582,17 +612,16 @@ def per_workload(args):
                                               ws, st)
         scat_f = lambda: uep.ultraep_dispatch_scatter(x, T, k, H, ros, boff[-1:], send)
         pack_f = lambda: uep.ultraep_pack_replicas(w, W, rank, g, plan, stg, cap, doff, st)
-        rec = {"workload": c.name, "R": c.R, "E": c.E, "n_slot": c.n_slot, "k": k, "T": T,
-               "H": H, "F": c.F, "rank": rank, "replicas_shipped": outb[rank]}
-        rec["count_us"] = round(graph_us([count_f]), 2)
-        rec["plan_us"] = round(graph_us([plan_f]), 2)
-        rec["count_plan_us"] = round(graph_us([count_f, plan_f]), 2)
-        rec["replicate_us"] = round(graph_us([lambda: uep.ultraep_plan_replicate(load, g, plan)]), 2)
-        rec["reroute_us"] = round(graph_us([lambda: uep.ultraep_plan_reroute(load, g, plan)]), 2)
+        rec = {"workload": c.name, "m": m, "rank": rank, "replicas_shipped": outb[rank]}
+        rec["count_us"] = graph_us([count_f])
+        rec["plan_us"] = graph_us([plan_f])
+        rec["count_plan_us"] = graph_us([count_f, plan_f])
+        rec["replicate_us"] = graph_us([lambda: uep.ultraep_plan_replicate(load, g, plan)])
+        rec["reroute_us"] = graph_us([lambda: uep.ultraep_plan_reroute(load, g, plan)])
         rec["max_hosts"] = int(plan.stats[5].item())
-        rec["dispatch_us"] = round(ev_us([disp_f]), 2)
-        rec["scatter_us"] = round(ev_us([scat_f]), 2)
-        rec["pack_us"] = round(ev_us([pack_f]), 2) if outb[rank] else 0.0
+        rec["dispatch_us"] = cold_us(disp_f, n_cold)
+        rec["scatter_us"] = cold_us(scat_f, n_cold)
+        rec["pack_us"] = cold_us(pack_f, n_cold) if outb[rank] else None
         torch.cuda.synchronize()
         assert int(st.item()) == 0, int(st.item())
         n_routed = int(boff[-1].item())
@@ -601,14 +630,15 @@ def per_workload(args):
                           minlength=c.n_main)
         pb = int(sum(2 * W * (1 + f) for f in fan if f > 0))
         rec["scatter_bytes"] = sb
-        rec["scatter_GBps"] = round(sb / rec["scatter_us"] / 1e3, 1)
+        rec["scatter_GBps"] = round(sb / rec["scatter_us"]["median"] / 1e3, 1)
         rec["pack_bytes"] = pb
-        rec["pack_GBps"] = round(pb / rec["pack_us"] / 1e3, 1) if pb else None
+        rec["pack_GBps"] = round(pb / rec["pack_us"]["median"] / 1e3, 1) if pb else None
         # the oracle, single-threaded, once each, on the same inputs
         (ocnt, _), t_cnt = wall_us(lambda: oracle.count(tk_all, c.E, c.R))
         op, t_plan = wall_us(lambda: oracle.plan(ocnt, og))
-        (osend, oros, oboff, _), t_disp = wall_us(lambda: oracle.dispatch(x_h, tk_all[rank], rank, og, op))
-        (ostg, odoff, n_out, _), t_pack = wall_us(lambda: oracle.pack(w_h, rank, og, op, cap))
+        (osend, oros, oboff, _), t_disp = wall_us(
+            lambda: oracle.dispatch(xw["x_h"], tk_all[rank], rank, og, op))
+        (ostg, odoff, n_out, _), t_pack = wall_us(lambda: oracle.pack(xw["w_h"], rank, og, op, cap))
         exact = (np.array_equal(load.cpu().numpy(), ocnt)
                  and all(np.array_equal(getattr(plan, f).cpu().numpy().reshape(-1),
                                         getattr(op, f).reshape(-1)) for f in uep.PLAN_FIELDS)
@@ -617,12 +647,68 @@ def per_workload(args):
                  and np.array_equal(send.cpu().numpy().view(np.uint16), osend)
                  and np.array_equal(doff.cpu().numpy(), odoff)
                  and np.array_equal(stg[:n_out].cpu().numpy().view(np.uint16), ostg[:n_out]))
-        rec["oracle_us"] = {"count_all_ranks": round(t_cnt, 1), "count_one_rank": round(t_cnt / c.R, 1),
-                            "plan": round(t_plan, 1), "dispatch": round(t_disp, 1),
-                            "pack": round(t_pack, 1), "cores": 1}
+        rec["oracle_us"] = {"count_all_ranks": t_cnt, "count_one_rank": round(t_cnt / c.R, 1),
+                            "plan": t_plan, "dispatch": t_disp, "pack": t_pack, "cores": 1}
         rec["bit_exact"] = bool(exact)
-        print(json.dumps(rec), flush=True)
-        del x, w, send, stg, tk_d, plan, load
+        del osend, ostg
+        return rec, (tk_r, load, plan, rank)
+
+    for cid in sorted(gen.CONFIGS):
+        c = gen.config(cid)
+        g = uep.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+        og = oracle.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+        shape = {"R": c.R, "E": c.E, "n_slot": c.n_slot, "k": c.k, "T": c.T, "H": c.H, "F": c.F}
+        ms = list(range(c.n_micro)) if cid in (3, 5) else [0]
+        n_cold = 20 if cid == 5 else 50
+        xw, recs, keep = {}, [], []
+        for m in ms:
+            rec, kp = instance(c, m, g, og, xw, n_cold)
+            if m == 0:
+                rec.update(shape)
+            recs.append(rec)
+            if cid == 5:
+                keep.append(kp)
+            print(json.dumps(rec), flush=True)
+        if len(ms) > 1:
+            med = lambda key, sub=None: round(float(np.median(
+                [r[key][sub] if sub else r[key] for r in recs])), 2)
+            summ = {"workload": c.name, "instances": len(ms), **shape,
+                    "median": {"count_us": med("count_us"), "plan_us": med("plan_us"),
+                               "count_plan_us": med("count_plan_us"),
+                               "replicate_us": med("replicate_us"), "reroute_us": med("reroute_us"),
+                               "dispatch_us": med("dispatch_us", "median"),
+                               "scatter_us": med("scatter_us", "median"),
+                               "pack_us": round(float(np.median([r["pack_us"]["median"] for r in recs
+                                                                 if r["pack_us"]])), 2),
+                               "scatter_GBps": med("scatter_GBps")},
+                    "max": {"count_plan_us": max(r["count_plan_us"] for r in recs),
+                            "max_hosts": max(r["max_hosts"] for r in recs)},
+                    "bit_exact_all": all(r["bit_exact"] for r in recs)}
+            if cid == 5:
+                # count + plan of every layer back to back: one graph, 58 pairs
+                st = torch.zeros(1, dtype=torch.int32, device=dev)
+                fns = []
+                for tk_r, load, plan, rank in keep:
+                    fns.append(lambda tk_r=tk_r, load=load, rank=rank: uep.ultraep_count(
+                        tk_r, c.T, c.k, c.E, 1, load[rank], st))
+                    fns.append(lambda load=load, plan=plan: uep.ultraep_plan(load, g, plan))
+                tot = graph_us(fns, n=1)
+                assert int(st.item()) == 0
+                summ["all_layers_count_plan_us"] = {"total": tot, "per_layer": round(tot / len(ms), 2)}
+            print(json.dumps({"summary": summ}), flush=True)
+        del xw, recs, keep
+        torch.cuda.empty_cache()
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(c, tk_all, rank, x_h, w_h, cap, budget_s):
@@ -661,6 +747,7 @@ def cpu_baseline(c, tk_all, rank, x_h, w_h, cap, budget_s):
         "sample": (f"{n} full steps of the same workload and rank (count, plan, "
                    f"dispatch with row copies, pack with blob copies), "
                    f"{tot:.1f} s of single-threaded C on {os.cpu_count()} host cores"),
+        "cpu_model": cpu_model(),
         "parts_us": {kk: round(v / n * 1e6, 1) for kk, v in parts.items()},
     }
 
