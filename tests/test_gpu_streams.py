@@ -1,0 +1,108 @@
+"""Reentrancy across streams: the library keeps no state between calls, so
+two complete pipelines (count, plan, dispatch, pack, relay trees, combine)
+with their own buffers, launched interleaved call by call on two streams,
+must each give the oracle's bytes.  Both streams keep the default priority.
+Needs an MI355X."""
+import numpy as np
+import pytest
+import torch
+
+import gen
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import gpu_path as gp
+    import paper_2606_04101_amd as uep
+
+
+class Pipe:
+    """One workload's buffers and its calls, in order."""
+
+    def __init__(self, cid, m, W):
+        c = gen.config(cid)
+        self.c, self.m, self.W = c, m, W
+        self.g, self.og = gp.groups(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+        self.tk_all = gen.topk_all(c, m)
+        load, _ = oracle.count(self.tk_all, c.E, c.R)
+        self.op = oracle.plan(load, self.og)
+        X = self.op.slot_expert
+        outb = [int(((X >= 0) & (X // c.n_main == r)).sum()) for r in range(c.R)]
+        self.rank = int(np.argmax(outb))
+        self.x_h = gen.activations(c, m, self.rank)
+        self.w_h = gen.weights(c, self.rank, W=W)
+        rng = np.random.default_rng(cid * 100 + m)
+        self.gate_h = rng.random((c.T, c.k)).astype(np.float32)
+        T, k, H, g = c.T, c.k, c.H, self.g
+        V = T * k
+        dev = gp.DEV
+        self.tk_d = gp.dev_i32(self.tk_all)
+        self.tk_r = self.tk_d[self.rank].contiguous()
+        self.x, self.w = gp.dev_u16(self.x_h), gp.dev_u16(self.w_h)
+        self.gate = torch.from_numpy(self.gate_h).to(dev)
+        self.st = gp.zero_status()
+        self.load = torch.empty((c.R, c.E), dtype=torch.int32, device=dev)
+        self.plan = uep.Plan(g, dev)
+        self.send = torch.empty((V, H), dtype=torch.int16, device=dev)
+        self.ros = torch.empty(V, dtype=torch.int32, device=dev)
+        self.boff = torch.empty(c.R * g.S + 1, dtype=torch.int64, device=dev)
+        self.ws = torch.empty(uep.ultraep_dispatch_ws_bytes(T, k, g), dtype=torch.uint8, device=dev)
+        self.cap = c.R * c.n_slot
+        self.stg = torch.zeros((self.cap, W), dtype=torch.int16, device=dev)
+        self.doff = torch.empty(c.R + 1, dtype=torch.int64, device=dev)
+        self.src = torch.empty(max(c.R * c.n_slot, 1), dtype=torch.int32, device=dev)
+        self.vol = torch.empty(c.R, dtype=torch.int32, device=dev)
+        self.rst = torch.empty(4, dtype=torch.int64, device=dev)
+        self.out = torch.empty((T, H), dtype=torch.int16, device=dev)
+
+    def calls(self):
+        c, g, p = self.c, self.g, self
+        T, k, H, V = c.T, c.k, c.H, c.T * c.k
+        return [
+            lambda: uep.ultraep_count(p.tk_d, T, k, c.E, c.R, p.load, p.st),
+            lambda: uep.ultraep_plan(p.load, g, p.plan),
+            lambda: uep.ultraep_dispatch(p.x, p.tk_r, T, k, H, p.rank, g, p.plan, p.send, p.ros,
+                                         p.boff, p.ws, p.st),
+            lambda: uep.ultraep_pack_replicas(p.w, p.W, p.rank, g, p.plan, p.stg, p.cap, p.doff,
+                                              p.st),
+            lambda: uep.ultraep_relay_plan(g, p.plan, 4, p.src, p.vol, p.rst, p.st),
+            lambda: uep.ultraep_combine(p.send, V, p.gate, p.ros, T, k, H, p.out, p.st),
+        ]
+
+    def check(self):
+        c = self.c
+        assert int(self.st.item()) == 0
+        ocnt, _ = oracle.count(self.tk_all, c.E, c.R)
+        assert np.array_equal(self.load.cpu().numpy(), ocnt)
+        gp.assert_plan_equal(self.plan, self.op)
+        osend, oros, oboff, _ = oracle.dispatch(self.x_h, self.tk_all[self.rank], self.rank,
+                                                self.og, self.op)
+        assert np.array_equal(self.ros.cpu().numpy(), oros)
+        assert np.array_equal(self.boff.cpu().numpy(), oboff)
+        assert np.array_equal(gp.host_u16(self.send), osend)
+        ostg, odoff, n_out, _ = oracle.pack(self.w_h, self.rank, self.og, self.op, self.cap)
+        assert np.array_equal(self.doff.cpu().numpy(), odoff)
+        assert np.array_equal(gp.host_u16(self.stg)[:n_out], ostg[:n_out])
+        rel = oracle.relay(self.og, self.op, 4)
+        assert np.array_equal(self.src.cpu().numpy()[: c.R * c.n_slot].reshape(c.R, c.n_slot),
+                              rel.slot_src.reshape(c.R, c.n_slot))
+        assert np.array_equal(self.vol.cpu().numpy(), rel.send_vol)
+        oout, _ = oracle.combine(osend, self.gate_h, oros)
+        assert np.array_equal(gp.host_u16(self.out), oout)
+
+
+def test_two_pipelines_on_two_streams():
+    pipes = [Pipe(2, 0, 8 * 4096), Pipe(3, 4, 8 * 4096)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())  # inputs were written on the default stream
+    calls = [p.calls() for p in pipes]
+    for rep in range(3):
+        for pair in zip(*calls):
+            for s, f in zip(streams, pair):
+                with torch.cuda.stream(s):
+                    f()
+    torch.cuda.synchronize()
+    for p in pipes:
+        p.check()
