@@ -637,7 +637,7 @@ def per_workload(args):
         (ocnt, _), t_cnt = wall_us(lambda: oracle.count(tk_all, c.E, c.R))
         op, t_plan = wall_us(lambda: oracle.plan(ocnt, og))
         (osend, oros, oboff, _), t_disp = wall_us(
-            lambda: oracle.dispatch(xw["x_h"], tk_all[rank], rank, og, op))
+            lambda: oracle.dispatch(xw["x_h"], tk_all[rank], rank, og, op, poison=False))
         (ostg, odoff, n_out, _), t_pack = wall_us(lambda: oracle.pack(xw["w_h"], rank, og, op, cap))
         exact = (np.array_equal(load.cpu().numpy(), ocnt)
                  and all(np.array_equal(getattr(plan, f).cpu().numpy().reshape(-1),
@@ -728,7 +728,7 @@ def cpu_baseline(c, tk_all, rank, x_h, w_h, cap, budget_s):
         load[rank] = row[0]
         p = oracle.plan(load, og)
         t2 = time.perf_counter()
-        _, _, _, st = oracle.dispatch(x_h, tk_r, rank, og, p)
+        _, _, _, st = oracle.dispatch(x_h, tk_r, rank, og, p, poison=False)
         t3 = time.perf_counter()
         _, _, _, st2 = oracle.pack(w_h, rank, og, p, cap)
         t4 = time.perf_counter()

@@ -200,15 +200,25 @@ def apportion(demand, ures):
     return out
 
 
-def dispatch(x, topk, rank, g: Group, p: Plan):
-    """-> send [T*k, H] uint16, row_of_slot [T*k], block_off [R*S+1], status"""
+def dispatch(x, topk, rank, g: Group, p: Plan, poison=True):
+    """-> send [T*k, H] uint16, row_of_slot [T*k], block_off [R*S+1], status.
+    poison: hand orc_dispatch outputs filled with a pattern it must overwrite
+    (every row_of_slot entry, every block offset, every send row: the routed
+    rows and the zero tail), so a missed write shows; False hands it zeroed
+    buffers (the timed baseline, where filling 2 bytes per send element would
+    add host work the oracle itself does not do)."""
     x = _c(x, np.uint16)
     topk = _c(topk, np.int32)
     T, H = x.shape
     k = topk.shape[1] if topk.ndim == 2 else 1
-    send = np.zeros((T * k, H), np.uint16)
-    ros = np.full(T * k, -1, np.int32)
-    boff = np.zeros(g.R * g.S + 1, np.int64)
+    if poison:
+        send = np.full((T * k, H), 0xDEAD, np.uint16)
+        ros = np.full(T * k, -7, np.int32)
+        boff = np.full(g.R * g.S + 1, -7, np.int64)
+    else:
+        send = np.zeros((T * k, H), np.uint16)
+        ros = np.full(T * k, -1, np.int32)
+        boff = np.zeros(g.R * g.S + 1, np.int64)
     gc = g.c()
     X = p.slot_expert if p.slot_expert.size else np.zeros(1, np.int32)
     st = lib().orc_dispatch(_p(x), _p(topk), T, k, H, rank, ctypes.byref(gc),

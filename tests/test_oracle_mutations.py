@@ -13,6 +13,10 @@ import test_oracle_pins as pins
 SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                    "oracle", "oracle.c")
 
+# Not listed: dropping the probe's "expert already on t" guard.  After a
+# transfer of e to t either t's slack is spent (delta = slack) or e's loop
+# ends (delta = excess or cap), so the guard never decides a target and the
+# mutant is equivalent (the oracle asserts this as its lemma flag).
 MUTATIONS = {
     "argmax_tie_to_higher_rank": ("if (best < 0 || slk[t] > slk[best]) best = t;",
                                   "if (best < 0 || slk[t] >= slk[best]) best = t;"),
@@ -72,6 +76,20 @@ MUTATIONS = {
     "combine_accumulates_in_double": ("      volatile float acc = 0.0f; /* volatile",
                                       "      volatile double acc = 0.0f; /* volatile"),
     "grad_reduce_keeps_replicas": ("        rg[i] = 0.0f;\n", "\n"),
+    "count_skips_expert_zero": ("      if (e == -1) continue;\n      if (e < -1 || e >= E) { status = ORC_EDATA; continue; }\n      c[e] += 1;",
+                                "      if (e <= 0) continue;\n      if (e < -1 || e >= E) { status = ORC_EDATA; continue; }\n      c[e] += 1;"),
+    "probe_slack_not_consumed": ("        slk[best] -= delta;\n", "\n"),
+    "probe_excess_not_consumed": ("        exc[r] -= delta;\n", "\n"),
+    "bisect_keeps_failed_tau": ("      lo = tau + 1;", "      lo = tau;"),
+    "bisect_forgets_best": ("      if (U) memcpy(U, Ut, sizeof(int64_t) * (size_t)g->E * g->R);\n",
+                            "\n"),
+    "dispatch_copies_next_token": ("memcpy(send + (int64_t)row_of_slot[i] * H, x + (i / k) * H,",
+                                   "memcpy(send + (int64_t)row_of_slot[i] * H, x + ((i / k + 1) % T) * H,"),
+    "dispatch_tail_not_zeroed": ("    if (V > v_valid)\n      memset(", "    if (0)\n      memset("),
+    "block_off_starts_at_first_block_size": ("  block_off[0] = 0;\n  for (int64_t b = 0; b < (int64_t)R * S; b++) block_off[b + 1]",
+                                             "  block_off[0] = cnt[0];\n  for (int64_t b = 0; b < (int64_t)R * S; b++) block_off[b + 1]"),
+    "pack_counts_other_ranks_experts": ("    dest_off[t] = n;\n    for (int32_t s = 0; s < NS; s++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e >= 0 && home(g, e) == rank) n++;\n    }\n  }\n  dest_off[R] = n;\n  *n_out = n;\n  if (n > cap) return ORC_ENOSPC;\n  if (n > 0 && !staging) return ORC_EINVAL;",
+                                        "    dest_off[t] = n;\n    for (int32_t s = 0; s < NS; s++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e >= 0) n++;\n    }\n  }\n  dest_off[R] = n;\n  *n_out = n;\n  if (n > cap) return ORC_ENOSPC;\n  if (n > 0 && !staging) return ORC_EINVAL;"),
     "grad_reduce_slot_major": (
         "  n = 0;\n  for (int32_t t = 0; t < R; t++)\n    for (int32_t s = 0; s < NS; s++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e < 0 || home(g, e) != rank) continue;\n      float *mg",
         "  n = 0;\n  for (int32_t s = 0; s < NS; s++)\n    for (int32_t t = 0; t < R; t++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e < 0 || home(g, e) != rank) continue;\n      float *mg"),
