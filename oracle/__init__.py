@@ -166,13 +166,14 @@ def plan(load, g: Group, locality=True) -> Plan:
     assert load.shape == (g.R, g.E)
     ns = max(g.n_slot, 0)
     ncol = g.E + g.R * ns
-    X = np.full((g.R, ns), -1, np.int32)
-    U = np.zeros((g.E, g.R), np.int32)
-    hp = np.zeros(g.E + 1, np.int32)
-    hr = np.full(ncol, -1, np.int32)
-    hs = np.full(ncol, -1, np.int32)
-    q = np.zeros((g.R, ncol), np.int32)
-    stats = np.zeros(8, np.int64)
+    # poisoned outputs: orc_plan must write every element, padding included
+    X = np.full((g.R, ns), -7, np.int32)
+    U = np.full((g.E, g.R), -7, np.int32)
+    hp = np.full(g.E + 1, -7, np.int32)
+    hr = np.full(ncol, -7, np.int32)
+    hs = np.full(ncol, -7, np.int32)
+    q = np.full((g.R, ncol), -7, np.int32)
+    stats = np.full(8, -7, np.int64)
     gc = g.c()
     st = lib().orc_plan(_p(load), ctypes.byref(gc), int(bool(locality)),
                         _p(X) if X.size else _p(np.zeros(1, np.int32)),
@@ -294,7 +295,7 @@ def combine(y, gate, row_of_slot):
     T, k = gate.shape
     ros = _c(row_of_slot, np.int32).reshape(-1)
     n_rows, H = y.shape
-    out = np.zeros((T, H), np.uint16)
+    out = np.full((T, H), 0xDEAD, np.uint16)  # poisoned: every output row must be written
     st = lib().orc_combine(_p(y) if y.size else None, _p(gate), _p(ros), T, k, H, n_rows,
                            _p(out))
     return out, st
