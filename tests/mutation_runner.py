@@ -22,7 +22,7 @@ def main(lib_path, bf_exe):
         lambda: [pins.test_worked_example_plan(orc, n) for n in
                  ("W0_single_hot_expert.json", "W1_nonmonotone_bisection.json",
                   "W2_proportional_split.json", "W4_two_slots_dispatch_pack.json",
-                  "W5_visit_order.json")],
+                  "W5_visit_order.json", "W7_source_order.json")],
         lambda: pins.test_w6_pack_order(orc),
         lambda: pins.test_w1_feasibility_is_not_monotone(orc),
         lambda: pins.test_w3_rounding_keeps_both_margins(orc),

@@ -88,6 +88,12 @@ MUTATIONS = {
     "dispatch_tail_not_zeroed": ("    if (V > v_valid)\n      memset(", "    if (0)\n      memset("),
     "block_off_starts_at_first_block_size": ("  block_off[0] = 0;\n  for (int64_t b = 0; b < (int64_t)R * S; b++) block_off[b + 1]",
                                              "  block_off[0] = cnt[0];\n  for (int64_t b = 0; b < (int64_t)R * S; b++) block_off[b + 1]"),
+    "x_slots_fill_from_the_end": ("        slots[(int64_t)best * NS + used[best]] = e;",
+                                  "        slots[(int64_t)best * NS + (NS - 1 - used[best])] = e;"),
+    "hosts_in_descending_rank_order": ("    for (int32_t t = 0; t < R; t++)\n      for (int32_t s = 0; s < NS; s++)\n        if (X[(int64_t)t * NS + s] == e) {",
+                                       "    for (int32_t t = R - 1; t >= 0; t--)\n      for (int32_t s = 0; s < NS; s++)\n        if (X[(int64_t)t * NS + s] == e) {"),
+    "residual_sources_descending": ("    for (int32_t r = 0; r < R; r++) {\n      if (lamhat[r] == 0) continue;",
+                                    "    for (int32_t r = R - 1; r >= 0; r--) {\n      if (lamhat[r] == 0) continue;"),
     "pack_counts_other_ranks_experts": ("    dest_off[t] = n;\n    for (int32_t s = 0; s < NS; s++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e >= 0 && home(g, e) == rank) n++;\n    }\n  }\n  dest_off[R] = n;\n  *n_out = n;\n  if (n > cap) return ORC_ENOSPC;\n  if (n > 0 && !staging) return ORC_EINVAL;",
                                         "    dest_off[t] = n;\n    for (int32_t s = 0; s < NS; s++) {\n      int32_t e = slot_expert[(int64_t)t * NS + s];\n      if (e >= 0) n++;\n    }\n  }\n  dest_off[R] = n;\n  *n_out = n;\n  if (n > cap) return ORC_ENOSPC;\n  if (n > 0 && !staging) return ORC_EINVAL;"),
     "grad_reduce_slot_major": (

@@ -31,7 +31,7 @@ def group_of(orc, d):
                                   "W1_nonmonotone_bisection.json",
                                   "W2_proportional_split.json",
                                   "W4_two_slots_dispatch_pack.json",
-                                  "W5_visit_order.json"])
+                                  "W5_visit_order.json", "W7_source_order.json"])
 def test_worked_example_plan(orc, name):
     d = load_golden(name)
     g = group_of(orc, d)
