@@ -524,7 +524,6 @@ def per_workload(args):
     import torch
 
     import gen
-    import oracle
     import paper_2606_04101_amd as uep
 
     dev = torch.device("cuda:0")
@@ -571,12 +570,7 @@ def per_workload(args):
             ts.append(1e3 * e0.elapsed_time(e1) / n)
         return round(float(np.median(ts)), 2)
 
-    def wall_us(f):
-        t0 = time.perf_counter()
-        r = f()
-        return r, round(1e6 * (time.perf_counter() - t0), 1)
-
-    def instance(c, m, g, og, xw, n_cold):
+    def instance(c, m, g, xw, n_cold):
         """One microbatch / layer m of workload c; xw holds the activations and
         weights (host and device) of the first instance's measured rank."""
         T, k, H, W = c.T, c.k, c.H, c.W
@@ -633,36 +627,32 @@ def per_workload(args):
         rec["scatter_GBps"] = round(sb / rec["scatter_us"]["median"] / 1e3, 1)
         rec["pack_bytes"] = pb
         rec["pack_GBps"] = round(pb / rec["pack_us"]["median"] / 1e3, 1) if pb else None
-        # the oracle, single-threaded, once each, on the same inputs
-        (ocnt, _), t_cnt = wall_us(lambda: oracle.count(tk_all, c.E, c.R))
-        op, t_plan = wall_us(lambda: oracle.plan(ocnt, og))
-        (osend, oros, oboff, _), t_disp = wall_us(
-            lambda: oracle.dispatch(xw["x_h"], tk_all[rank], rank, og, op, poison=False))
-        (ostg, odoff, n_out, _), t_pack = wall_us(lambda: oracle.pack(xw["w_h"], rank, og, op, cap))
-        exact = (np.array_equal(load.cpu().numpy(), ocnt)
+        # the CPU baseline on the same inputs, and whether it agrees byte for byte
+        base = oracle_baseline(c, tk_all, rank, xw["x_h"], xw["w_h"], cap)
+        o = base["outputs"]
+        n_out = o["n_out"]
+        exact = (np.array_equal(load.cpu().numpy(), o["counts"])
                  and all(np.array_equal(getattr(plan, f).cpu().numpy().reshape(-1),
-                                        getattr(op, f).reshape(-1)) for f in uep.PLAN_FIELDS)
-                 and np.array_equal(ros.cpu().numpy(), oros)
-                 and np.array_equal(boff.cpu().numpy(), oboff)
-                 and np.array_equal(send.cpu().numpy().view(np.uint16), osend)
-                 and np.array_equal(doff.cpu().numpy(), odoff)
-                 and np.array_equal(stg[:n_out].cpu().numpy().view(np.uint16), ostg[:n_out]))
-        rec["oracle_us"] = {"count_all_ranks": t_cnt, "count_one_rank": round(t_cnt / c.R, 1),
-                            "plan": t_plan, "dispatch": t_disp, "pack": t_pack, "cores": 1}
+                                        o["plan"][f].reshape(-1)) for f in uep.PLAN_FIELDS)
+                 and np.array_equal(ros.cpu().numpy(), o["row_of_slot"])
+                 and np.array_equal(boff.cpu().numpy(), o["block_off"])
+                 and np.array_equal(send.cpu().numpy().view(np.uint16), o["send"])
+                 and np.array_equal(doff.cpu().numpy(), o["dest_off"])
+                 and np.array_equal(stg[:n_out].cpu().numpy().view(np.uint16), o["staging"][:n_out]))
+        rec["oracle_us"] = base["us"]
         rec["bit_exact"] = bool(exact)
-        del osend, ostg
+        del base, o
         return rec, (tk_r, load, plan, rank)
 
     for cid in sorted(gen.CONFIGS):
         c = gen.config(cid)
         g = uep.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
-        og = oracle.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
         shape = {"R": c.R, "E": c.E, "n_slot": c.n_slot, "k": c.k, "T": c.T, "H": c.H, "F": c.F}
         ms = list(range(c.n_micro)) if cid in (3, 5) else [0]
         n_cold = 20 if cid == 5 else 50
         xw, recs, keep = {}, [], []
         for m in ms:
-            rec, kp = instance(c, m, g, og, xw, n_cold)
+            rec, kp = instance(c, m, g, xw, n_cold)
             if m == 0:
                 rec.update(shape)
             recs.append(rec)
@@ -698,6 +688,31 @@ def per_workload(args):
             print(json.dumps({"summary": summ}), flush=True)
         del xw, recs, keep
         torch.cuda.empty_cache()
+
+
+def oracle_baseline(c, tk_all, rank, x_h, w_h, cap):
+    """The CPU-baseline leg of --workloads: the oracle (single-threaded C)
+    once on the same inputs as the GPU instance, each step wall-clock timed;
+    its outputs come back so the caller can report whether the GPU's agree."""
+    import oracle
+    import paper_2606_04101_amd as uep
+    og = oracle.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
+
+    def wall_us(f):
+        t0 = time.perf_counter()
+        r = f()
+        return r, round(1e6 * (time.perf_counter() - t0), 1)
+
+    (ocnt, _), t_cnt = wall_us(lambda: oracle.count(tk_all, c.E, c.R))
+    op, t_plan = wall_us(lambda: oracle.plan(ocnt, og))
+    (osend, oros, oboff, _), t_disp = wall_us(
+        lambda: oracle.dispatch(x_h, tk_all[rank], rank, og, op, poison=False))
+    (ostg, odoff, n_out, _), t_pack = wall_us(lambda: oracle.pack(w_h, rank, og, op, cap))
+    return {"us": {"count_all_ranks": t_cnt, "count_one_rank": round(t_cnt / c.R, 1),
+                   "plan": t_plan, "dispatch": t_disp, "pack": t_pack, "cores": 1},
+            "outputs": {"counts": ocnt, "plan": {f: getattr(op, f) for f in uep.PLAN_FIELDS},
+                        "row_of_slot": oros, "block_off": oboff, "send": osend,
+                        "dest_off": odoff, "staging": ostg, "n_out": n_out}}
 
 
 def cpu_model():
