@@ -1,5 +1,5 @@
-"""Invariants I1-I13 of the oracle on the five synthetic workloads and on a
-seeded corpus of small adversarial cases (no GPU)."""
+"""Invariants I1-I13 of the oracle on the five synthetic workloads, on a
+seeded corpus of small adversarial cases and on a mid-size corpus (no GPU)."""
 import numpy as np
 import pytest
 
@@ -75,6 +75,30 @@ def test_fuzz_case(orc, seed):
         assert st == 0
         check_dispatch(x, c["topk"][r], r, g, p, send, ros, boff)
         w = rng.integers(0, 2 ** 16, (g.n_main, c["W"])).astype(np.uint16)
+        staging, doff, n_out, st = orc.pack(w, r, g, p, g.R * g.n_slot)
+        assert st == 0
+        check_pack(w, r, g, p, staging, doff, n_out)
+
+
+@pytest.mark.parametrize("seed", range(0, 48))
+def test_mid_case(orc, seed):
+    """The mid-size corpus: up to 64 ranks, 1024 experts, top-64."""
+    c = fuzz.make_mid_case(seed)
+    g = orc.Group(c["R"], c["E"], c["n_slot"], c["u_min"], c["beta_num"],
+                  c["beta_den"])
+    load, st = orc.count(c["topk"], g.E, g.R)
+    assert st == 0
+    assert load.sum() == (c["topk"] >= 0).sum()
+    p = _plan_case(orc, load, g)
+    rng = c["rng"]
+    X = p.slot_expert.reshape(g.R, max(g.n_slot, 0))
+    outb = [int(((X >= 0) & (X // g.n_main == r)).sum()) for r in range(g.R)]
+    for r in sorted({0, int(np.argmax(outb)), g.R - 1}):
+        x = rng.integers(0, 2 ** 16, (c["T"], 8)).astype(np.uint16)
+        send, ros, boff, st = orc.dispatch(x, c["topk"][r], r, g, p)
+        assert st == 0
+        check_dispatch(x, c["topk"][r], r, g, p, send, ros, boff)
+        w = rng.integers(0, 2 ** 16, (g.n_main, 16)).astype(np.uint16)
         staging, doff, n_out, st = orc.pack(w, r, g, p, g.R * g.n_slot)
         assert st == 0
         check_pack(w, r, g, p, staging, doff, n_out)
