@@ -4,7 +4,8 @@ Thin ctypes binding of ``libultraep.so`` (C ABI in ``include/ultraep.h``).
 Every function has the name of the C entry point it calls and only marshals
 arguments: torch tensors supply device memory, torch's current HIP stream is
 used unless another one is given, and every step runs in the library's HIP
-kernels.  A missing library raises immediately; there is no fallback path.
+kernels.  Before a call it checks that every tensor is large enough for the
+shapes given, so a kernel never runs past a caller's buffer.  A missing library raises immediately; there is no fallback path.
 
 Reference: "UltraEP: Unleash MoE Training and Inference on Rack-Scale Nodes
 with Near-Optimal Load Balancing", arXiv 2606.04101 (Algorithm 1, Sec. 5-6).
@@ -132,6 +133,19 @@ def _ptr(t):
     return t.data_ptr() if t.numel() else None
 
 
+def _need(t, n, esize, name):
+    """Raises unless t holds at least n elements of esize bytes, so that no
+    kernel reads or writes past a caller's tensor (n <= 0 needs nothing)."""
+    if n <= 0:
+        return
+    if t is None:
+        raise ValueError(f"{name}: a device tensor of {n} elements is needed")
+    if t.element_size() != esize:
+        raise ValueError(f"{name}: expected {esize}-byte elements, got {t.dtype}")
+    if t.numel() < n:
+        raise ValueError(f"{name}: needs {n} elements, has {t.numel()}")
+
+
 def _stream(stream):
     if stream is not None:
         return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
@@ -162,6 +176,9 @@ class Plan:
 
 
 def ultraep_count(topk, T, k, E, n_groups, counts, status, stream=None):
+    _need(topk, n_groups * T * k, 4, "topk")
+    _need(counts, n_groups * E, 4, "counts")
+    _need(status, 1, 4, "status")
     return _check(lib().ultraep_count(_ptr(topk), T, k, E, n_groups,
                                       _ptr(counts), _ptr(status),
                                       _stream(stream)), "ultraep_count")
@@ -174,6 +191,7 @@ def ultraep_plan_ws_bytes(g: Group) -> int:
 def ultraep_plan(load, g: Group, plan: Plan, ws=None, stream=None):
     """ws: device workspace (defaults to the one the Plan object holds)."""
     ws = plan.ws if ws is None else ws
+    _need(load, g.R * g.E, 4, "load")
     return _check(lib().ultraep_plan(_ptr(load), ctypes.byref(g),
                                      ctypes.byref(plan.c), _ptr(ws),
                                      ws.numel() * ws.element_size(),
@@ -182,12 +200,14 @@ def ultraep_plan(load, g: Group, plan: Plan, ws=None, stream=None):
 
 def ultraep_plan_replicate(load, g: Group, plan: Plan, ws=None, stream=None):
     ws = plan.ws if ws is None else ws
+    _need(load, g.R * g.E, 4, "load")
     return _check(lib().ultraep_plan_replicate(
         _ptr(load), ctypes.byref(g), ctypes.byref(plan.c), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)), "ultraep_plan_replicate")
 
 
 def ultraep_plan_reroute(load, g: Group, plan: Plan, stream=None):
+    _need(load, g.R * g.E, 4, "load")
     return _check(lib().ultraep_plan_reroute(
         _ptr(load), ctypes.byref(g), ctypes.byref(plan.c), _stream(stream)),
         "ultraep_plan_reroute")
@@ -197,8 +217,18 @@ def ultraep_dispatch_ws_bytes(T, k, g: Group) -> int:
     return int(lib().ultraep_dispatch_ws_bytes(T, k, ctypes.byref(g)))
 
 
+def _layout_need(topk, T, k, g, row_of_slot, block_off, status):
+    _need(topk, T * k, 4, "topk")
+    _need(row_of_slot, T * k, 4, "row_of_slot")
+    _need(block_off, g.R * g.S + 1, 8, "block_off")
+    _need(status, 1, 4, "status")
+
+
 def ultraep_dispatch(x, topk, T, k, H, rank, g: Group, plan: Plan, send,
                      row_of_slot, block_off, ws, status, stream=None):
+    _need(x, T * H, 2, "x")
+    _need(send, T * k * H, 2, "send")
+    _layout_need(topk, T, k, g, row_of_slot, block_off, status)
     return _check(lib().ultraep_dispatch(
         _ptr(x), _ptr(topk), T, k, H, rank, ctypes.byref(g),
         ctypes.byref(plan.c), _ptr(send), _ptr(row_of_slot), _ptr(block_off),
@@ -208,6 +238,7 @@ def ultraep_dispatch(x, topk, T, k, H, rank, g: Group, plan: Plan, send,
 
 def ultraep_dispatch_layout(topk, T, k, rank, g: Group, plan: Plan,
                             row_of_slot, block_off, ws, status, stream=None):
+    _layout_need(topk, T, k, g, row_of_slot, block_off, status)
     return _check(lib().ultraep_dispatch_layout(
         _ptr(topk), T, k, rank, ctypes.byref(g), ctypes.byref(plan.c),
         _ptr(row_of_slot), _ptr(block_off), _ptr(ws),
@@ -218,13 +249,25 @@ def ultraep_dispatch_layout(topk, T, k, rank, g: Group, plan: Plan,
 def ultraep_dispatch_scatter(x, T, k, H, row_of_slot, n_routed, send,
                              stream=None):
     """n_routed: a one-element int64 device tensor (e.g. block_off[-1:])."""
+    _need(x, T * H, 2, "x")
+    _need(row_of_slot, T * k, 4, "row_of_slot")
+    _need(n_routed, 1 if T > 0 else 0, 8, "n_routed")
+    _need(send, T * k * H, 2, "send")
     return _check(lib().ultraep_dispatch_scatter(
         _ptr(x), T, k, H, _ptr(row_of_slot), _ptr(n_routed), _ptr(send),
         _stream(stream)), "ultraep_dispatch_scatter")
 
 
+def _pack_need(w_main, W, g, staging, cap, dest_off, status):
+    _need(w_main, g.n_main * W, 2, "w_main")
+    _need(staging, cap * W, 2, "staging")
+    _need(dest_off, g.R + 1, 8, "dest_off")
+    _need(status, 1, 4, "status")
+
+
 def ultraep_pack_replicas(w_main, W, rank, g: Group, plan: Plan, staging, cap,
                           dest_off, status, stream=None):
+    _pack_need(w_main, W, g, staging, cap, dest_off, status)
     return _check(lib().ultraep_pack_replicas(
         _ptr(w_main), W, rank, ctypes.byref(g), ctypes.byref(plan.c),
         _ptr(staging), cap, _ptr(dest_off), _ptr(status), _stream(stream)),
@@ -233,6 +276,8 @@ def ultraep_pack_replicas(w_main, W, rank, g: Group, plan: Plan, staging, cap,
 
 def ultraep_reroute_and_pack(load, g: Group, plan: Plan, w_main, W, rank, staging,
                              cap, dest_off, status, stream=None):
+    _need(load, g.R * g.E, 4, "load")
+    _pack_need(w_main, W, g, staging, cap, dest_off, status)
     return _check(lib().ultraep_reroute_and_pack(
         _ptr(load), ctypes.byref(g), ctypes.byref(plan.c), _ptr(w_main), W, rank,
         _ptr(staging), cap, _ptr(dest_off), _ptr(status), _stream(stream)),
@@ -241,6 +286,10 @@ def ultraep_reroute_and_pack(load, g: Group, plan: Plan, w_main, W, rank, stagin
 
 def ultraep_relay_plan(g: Group, plan: Plan, threshold, slot_src, send_vol,
                        relay_stats, status, stream=None):
+    _need(slot_src, g.R * g.n_slot, 4, "slot_src")
+    _need(send_vol, g.R, 4, "send_vol")
+    _need(relay_stats, 4, 8, "relay_stats")
+    _need(status, 1, 4, "status")
     return _check(lib().ultraep_relay_plan(
         ctypes.byref(g), ctypes.byref(plan.c), threshold, _ptr(slot_src),
         _ptr(send_vol), _ptr(relay_stats), _ptr(status), _stream(stream)),
@@ -249,6 +298,9 @@ def ultraep_relay_plan(g: Group, plan: Plan, threshold, slot_src, send_vol,
 
 def ultraep_pack_relay(w_main, relay_src, W, rank, g: Group, plan: Plan, slot_src,
                        staging, cap, dest_off, status, stream=None):
+    _pack_need(w_main, W, g, staging, cap, dest_off, status)
+    _need(relay_src, g.n_slot * W, 2, "relay_src")
+    _need(slot_src, g.R * g.n_slot, 4, "slot_src")
     return _check(lib().ultraep_pack_relay(
         _ptr(w_main), _ptr(relay_src), W, rank, ctypes.byref(g), ctypes.byref(plan.c),
         _ptr(slot_src), _ptr(staging), cap, _ptr(dest_off), _ptr(status),
@@ -256,6 +308,11 @@ def ultraep_pack_relay(w_main, relay_src, W, rank, g: Group, plan: Plan, slot_sr
 
 
 def ultraep_combine(y, n_rows, gate, row_of_slot, T, k, H, out, status, stream=None):
+    _need(y, n_rows * H, 2, "y")
+    _need(gate, T * k, 4, "gate")
+    _need(row_of_slot, T * k, 4, "row_of_slot")
+    _need(out, T * H, 2, "out")
+    _need(status, 1, 4, "status")
     return _check(lib().ultraep_combine(
         _ptr(y), n_rows, _ptr(gate), _ptr(row_of_slot), T, k, H, _ptr(out), _ptr(status),
         _stream(stream)), "ultraep_combine")
@@ -263,6 +320,9 @@ def ultraep_combine(y, n_rows, gate, row_of_slot, T, k, H, out, status, stream=N
 
 def ultraep_grad_reduce(main_grad, rgrad, W, rank, g: Group, plan: Plan, cap, status,
                         stream=None):
+    _need(main_grad, g.n_main * W, 4, "main_grad")
+    _need(rgrad, cap * W, 4, "rgrad")
+    _need(status, 1, 4, "status")
     return _check(lib().ultraep_grad_reduce(
         _ptr(main_grad), _ptr(rgrad), W, rank, ctypes.byref(g), ctypes.byref(plan.c), cap,
         _ptr(status), _stream(stream)), "ultraep_grad_reduce")
