@@ -94,7 +94,7 @@ def main():
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the "
               "balancing path is replicated per rank and its collectives are not "
-              "part of this build.", file=sys.stderr)
+              "implemented here.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
