@@ -644,7 +644,7 @@ def per_workload(args):
         del base, o
         return rec, (tk_r, load, plan, rank)
 
-    for cid in sorted(gen.CONFIGS):
+    for cid in sorted(gen.WORKLOADS):
         c = gen.config(cid)
         g = uep.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
         shape = {"R": c.R, "E": c.E, "n_slot": c.n_slot, "k": c.k, "T": c.T, "H": c.H, "F": c.F}

@@ -139,7 +139,7 @@ class Config:
 # follow Table 2 / Sec. 8.1 of the paper; the Zipf scales c are calibrated
 # once (gen/calibrate.py) so that microbatch 0 has the stated max/mean rank
 # load, then frozen here.
-CONFIGS = {
+WORKLOADS = {
     1: Config(1, "tiny", R=4, E=16, n_slot=2, k=2, T=512, H=256, F=512,
               u_min=32, bias="normal", bias_scale=1.5),
     2: Config(2, "glm45air_layer", R=32, E=128, n_slot=2, k=8, T=4096,
@@ -161,7 +161,7 @@ ZIPF_C = {2: None, 4: None}
 
 
 def config(cid: int) -> Config:
-    c = CONFIGS[cid]
+    c = WORKLOADS[cid]
     if c.bias == "zipf":
         cc = ZIPF_C[cid]
         if cc is None:

@@ -15,7 +15,7 @@ TARGET = {2: (2.0, 0.05), 4: (3.5, 0.1)}
 
 
 def imbalance(cid, c_val):
-    base = gen.CONFIGS[cid]
+    base = gen.WORKLOADS[cid]
     cfg = gen.Config(**{**base.__dict__, "bias_scale": c_val})
     return gen.rank_imbalance(cfg, gen.topk_all(cfg, 0))
 
