@@ -46,12 +46,18 @@ constexpr int64_t kMaxLoad = int64_t(1) << 30;
 constexpr int kNotReached = INT32_MIN;
 constexpr int kPrepThreads = 1024;
 constexpr int kHdr = 4 + 4 * kRounds;  // int64 header words
+constexpr int kHdrSpan = 16;           // the header's share of the workspace: one 128-byte line
 constexpr int kBitWords = (kNodes + 63) / 64;  // outcome bits per round
+// Copies of each round's outcome words, one 128-byte line each: probe b sets
+// its bit in copy b % kCopies, which spreads the round's atomics over
+// kCopies lines instead of one.
+constexpr int kCopies = 8;
+static_assert(kHdr <= kHdrSpan && kBitWords * 8 == 128, "outcome copies are whole lines");
 
 struct PlanWs {
   int64_t *hdr;        // [4] tau_lo0, tau_hi0, L, status, then per round j the
                        // bisection state after rounds 0..j: lo, hi, best, probes
-  uint64_t *bits;      // [kRounds][kBitWords] feasible probes, one bit per node
+  uint64_t *bits;      // [kRounds][kCopies][kBitWords] feasible probes, one bit per node
   int32_t *ell;        // [R]
   int32_t *rank_desc;  // [R] ranks by descending load (visiting order)
   int32_t *rank_asc;   // [R] ranks by ascending load (target order)
@@ -65,15 +71,16 @@ struct PlanWs {
 size_t plan_ws_bytes(int32_t R, int32_t E, int32_t NS) {
   const int64_t RS = static_cast<int64_t>(R) * NS;
   const int64_t ints = 3 * R + 3 * E + int64_t(kRounds) * kNodes * (1 + 2 * RS);
-  return static_cast<size_t>(kHdr * 8 + kRounds * kBitWords * 8 + (ints * 4 + 255) / 256 * 256);
+  return static_cast<size_t>(kHdrSpan * 8 + kRounds * kCopies * kBitWords * 8 +
+                             (ints * 4 + 255) / 256 * 256);
 }
 
 static PlanWs carve(void *ws, int32_t R, int32_t E, int32_t NS) {
   (void)NS;
   PlanWs w;
   w.hdr = static_cast<int64_t *>(ws);
-  w.bits = reinterpret_cast<uint64_t *>(w.hdr + kHdr);
-  int32_t *p = reinterpret_cast<int32_t *>(w.bits + kRounds * kBitWords);
+  w.bits = reinterpret_cast<uint64_t *>(w.hdr + kHdrSpan);
+  int32_t *p = reinterpret_cast<int32_t *>(w.bits + kRounds * kCopies * kBitWords);
   w.ell = p;
   p += R;
   w.rank_desc = p;
@@ -129,7 +136,7 @@ __global__ void __launch_bounds__(kPrepThreads) k_plan_prep(PlanArgs a) {
     s_L = 0;
     s_bad = 0;
   }
-  if (tid < kRounds * kBitWords) a.ws.bits[tid] = 0;
+  if (tid < kRounds * kCopies * kBitWords) a.ws.bits[tid] = 0;
   __syncthreads();
   // lambda_e: thread (part, e) sums rows part, part + parts, ... with up to
   // 16 loads in flight, the parts are then combined in LDS
@@ -511,6 +518,19 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// Round rd's outcome words, word w in lane w: the OR of its copies.
+__device__ __forceinline__ uint64_t outcome_words(const PlanArgs &a, int rd) {
+  const int lane = lane_id();
+  uint64_t v[kCopies];
+#pragma unroll
+  for (int c = 0; c < kCopies; ++c)
+    v[c] = lane < kBitWords ? a.ws.bits[(rd * kCopies + c) * kBitWords + lane] : 0;
+  uint64_t bw = 0;
+#pragma unroll
+  for (int c = 0; c < kCopies; ++c) bw |= v[c];
+  return bw;
+}
+
 // The sequential bisection through round rd's depth-kDepth subtree, from
 // state st, over the round's outcome bits (word w in lane w).
 __device__ __forceinline__ void walk_bits(uint64_t bw, int rd, BisState &st) {
@@ -543,8 +563,7 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
   const int64_t status = a.ws.hdr[3];
   const bool packed = a.ws.hdr[1] < (int64_t(1) << 25);
   BisState st = state_before(a, round > 0 ? round - 1 : 0);
-  const uint64_t bw =
-      (round > 0 && lane < kBitWords) ? a.ws.bits[(round - 1) * kBitWords + lane] : 0;
+  const uint64_t bw = round > 0 ? outcome_words(a, round - 1) : 0;
   int ve[kMaxE / kWave], vl[kMaxE / kWave];
 #pragma unroll
   for (int u = 0; u < kMaxE / kWave; ++u) {
@@ -604,7 +623,9 @@ __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
   }
   if (lane == 0) {
     a.ws.res[round * kNodes + b] = n;
-    if (n >= 0) atomicOr(a.ws.bits + round * kBitWords + (b >> 6), uint64_t(1) << (b & 63));
+    if (n >= 0)
+      atomicOr(a.ws.bits + (round * kCopies + (b % kCopies)) * kBitWords + (b >> 6),
+               uint64_t(1) << (b & 63));
   }
 }
 
@@ -893,7 +914,7 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   const int64_t status = a.ws.hdr[3], L = a.ws.hdr[2];
   const int64_t lo0 = a.ws.hdr[0], hi0 = a.ws.hdr[1];
   BisState fin = state_before(a, kRounds - 1);
-  const uint64_t bw = lane < kBitWords ? a.ws.bits[(kRounds - 1) * kBitWords + lane] : 0;
+  const uint64_t bw = outcome_words(a, kRounds - 1);
   const int lam_e = a.ws.lam[e];
   const int lam_r = kReroute && lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
   if (status != 0) {
