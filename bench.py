@@ -696,6 +696,7 @@ def oracle_baseline(c, tk_all, rank, x_h, w_h, cap):
     its outputs come back so the caller can report whether the GPU's agree."""
     import oracle
     import paper_2606_04101_amd as uep
+    oracle.lib()  # loaded before the clock starts
     og = oracle.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
 
     def wall_us(f):
