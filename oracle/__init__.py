@@ -18,7 +18,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+_BUILT = os.path.join(_HERE, "liboracle.so")
+# ULTRAEP_ORACLE_LIB names another build of oracle.c (the sanitizer test's)
+_LIB = os.environ.get("ULTRAEP_ORACLE_LIB") or _BUILT
 
 OK, EINVAL, ENOSPC, EDATA, ELEMMA = 0, -1, -2, -4, -6
 
@@ -28,10 +30,10 @@ def build() -> str:
     # -ffp-contract=off: no fused multiply-add in the fp32 combine and
     # reduction (each product and sum rounds on its own)
     cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off",
-           "-fPIC", "-shared", "-o", _LIB + ".tmp", _SRC]
+           "-fPIC", "-shared", "-o", _BUILT + ".tmp", _SRC]
     subprocess.run(cmd, check=True, cwd=_HERE)
-    os.replace(_LIB + ".tmp", _LIB)
-    return _LIB
+    os.replace(_BUILT + ".tmp", _BUILT)
+    return _BUILT
 
 
 class _Group(ctypes.Structure):

@@ -16,7 +16,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libultraep.so")
+# the in-tree build; ULTRAEP_LIB names another build of the same sources
+# (for example a kernel variant under comparison) without replacing it
+LIB_PATH = os.environ.get("ULTRAEP_LIB") or os.path.join(_HERE, "libultraep.so")
 
 ULTRAEP_OK = 0
 ULTRAEP_EINVAL = -1

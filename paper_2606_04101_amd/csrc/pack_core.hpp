@@ -62,7 +62,7 @@ __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t 
   __shared__ int32_t s_gstart[kPkMaxLocal];    //                   first s_dst index
   __shared__ int32_t s_gli[kPkMaxEnt];         // per group: local expert
   __shared__ int32_t s_wcnt[kPkWaves];
-  __shared__ int32_t s_ngrp, s_off;
+  __shared__ int32_t s_off;
 
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int RS = a.R * a.NS;
@@ -88,10 +88,7 @@ __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t 
   const bool valid = li >= 0;
   const uint64_t bv = ballot(valid);
   if (lane == 0) s_wcnt[wave] = __popcll(bv);
-  if (tid == 0) {
-    s_ngrp = 0;
-    s_off = 0;
-  }
+  if (tid == 0) s_off = 0;
   __syncthreads();
   // staging entry of this slot: valid slots before it (destination rank
   // ascending, then slot)
@@ -119,13 +116,16 @@ __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t 
   __syncthreads();
   if (fidx == 0) s_gstart[li] = atomicAdd(&s_off, s_cnt[li]);
   // the groups themselves in ascending local-expert order, the same in
-  // every workgroup, since tasks are numbered by group
+  // every workgroup, since tasks are numbered by group; every thread keeps
+  // the running group count in a register (the pass totals are read from
+  // LDS by all threads between the same two barriers)
+  int ngrp = 0;
   for (int l0 = 0; l0 < nsrc; l0 += kPkThreads) {
     const int l = l0 + tid;
     const bool has = l < nsrc && s_cnt[l] > 0;
     const uint64_t hb = ballot(has);
-    int gi = s_ngrp + popc_below(hb);
-    __syncthreads();
+    int gi = ngrp + popc_below(hb);
+    __syncthreads();  // the previous pass has read s_wcnt
     if (lane == 0) s_wcnt[wave] = __popcll(hb);
     __syncthreads();
     int tot = 0;
@@ -134,12 +134,10 @@ __device__ __forceinline__ void pack_block(const PkArgs &a, int64_t wg, int64_t 
       tot += s_wcnt[w];
     }
     if (has) s_gli[gi] = l;
-    __syncthreads();
-    if (tid == 0) s_ngrp += tot;
+    ngrp += tot;
   }
   if (valid) s_dst[s_gstart[li] + fidx] = entry;
   __syncthreads();
-  const int ngrp = s_ngrp;
   const int64_t ntile = (a.nch + kPkTileCh - 1) / kPkTileCh;
   const int64_t ntask = ntile * ngrp;
   for (int64_t task = wg; task < ntask; task += n_wg) {

@@ -58,7 +58,7 @@ __global__ void __launch_bounds__(kRdThreads) k_grad_reduce(RdArgs a) {
   __shared__ int32_t s_gstart[kRdMaxLocal];  //                   first s_dst index
   __shared__ int32_t s_gli[kRdMaxEnt];       // per group: local expert
   __shared__ int32_t s_wcnt[kRdWaves];
-  __shared__ int32_t s_ngrp, s_off;
+  __shared__ int32_t s_off;
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int RS = a.R * a.NS;
   for (int l = tid; l < a.nm; l += kRdThreads) s_cnt[l] = 0;
@@ -71,10 +71,7 @@ __global__ void __launch_bounds__(kRdThreads) k_grad_reduce(RdArgs a) {
   const uint64_t bv = ballot(valid);
   if (lane == 0) s_wcnt[wave] = __popcll(bv);
   if (tid < kRdMaxEnt) s_li[tid] = li;
-  if (tid == 0) {
-    s_ngrp = 0;
-    s_off = 0;
-  }
+  if (tid == 0) s_off = 0;
   __syncthreads();
   // staging entry of this slot (destination rank, then slot) and the number
   // of replicas in all
@@ -95,13 +92,15 @@ __global__ void __launch_bounds__(kRdThreads) k_grad_reduce(RdArgs a) {
   if (valid) atomicAdd(&s_cnt[li], 1);
   __syncthreads();
   if (valid && pos == 0) s_gstart[li] = atomicAdd(&s_off, s_cnt[li]);
-  // groups in ascending local-expert order, the same in every workgroup
+  // groups in ascending local-expert order, the same in every workgroup;
+  // every thread keeps the running group count in a register
+  int ngrp = 0;
   for (int l0 = 0; l0 < a.nm; l0 += kRdThreads) {
     const int l = l0 + tid;
     const bool has = l < a.nm && s_cnt[l] > 0;
     const uint64_t hb = ballot(has);
-    int gi = s_ngrp + popc_below(hb);
-    __syncthreads();
+    int gi = ngrp + popc_below(hb);
+    __syncthreads();  // the previous pass has read s_wcnt
     if (lane == 0) s_wcnt[wave] = __popcll(hb);
     __syncthreads();
     int tot = 0;
@@ -110,12 +109,10 @@ __global__ void __launch_bounds__(kRdThreads) k_grad_reduce(RdArgs a) {
       tot += s_wcnt[w];
     }
     if (has) s_gli[gi] = l;
-    __syncthreads();
-    if (tid == 0) s_ngrp += tot;
+    ngrp += tot;
   }
   if (valid) s_dst[s_gstart[li] + pos] = entry;
   __syncthreads();
-  const int ngrp = s_ngrp;
   const int64_t ntile = (a.nch + kRdTileCh - 1) / kRdTileCh;
   const int64_t ntask = ntile * ngrp;
   const v4u z = v4u{0u, 0u, 0u, 0u};

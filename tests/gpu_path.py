@@ -59,6 +59,23 @@ def gpu_plan(load, g, split=False):
     return plan
 
 
+def assert_same(name, gpu, orc, limit=6):
+    """Raises unless the two arrays are equal, naming the number of differing
+    elements and the first ones by index, with the GPU and oracle values."""
+    gpu, orc = np.asarray(gpu), np.asarray(orc)
+    if gpu.shape != orc.shape:
+        raise AssertionError(f"{name}: shape {gpu.shape} against the oracle's {orc.shape}")
+    if np.array_equal(gpu, orc):
+        return
+    bad = np.argwhere(gpu != orc)
+    first = [(tuple(int(v) for v in ix), gpu[tuple(ix)].item(), orc[tuple(ix)].item())
+             for ix in bad[:limit]]
+    rows = np.unique(bad[:, 0]) if gpu.ndim > 1 else None
+    more = f" in {rows.size} rows (first rows {rows[:8].tolist()})" if rows is not None else ""
+    raise AssertionError(f"{name}: {len(bad)} of {gpu.size} elements differ{more}; "
+                         f"first (index, gpu, oracle): {first}")
+
+
 def assert_plan_equal(plan, op):
     for f in uep.PLAN_FIELDS:
         a = getattr(plan, f).cpu().numpy().reshape(-1)
@@ -104,15 +121,15 @@ def check_rank(x, topk, w, rank, g, og, plan, op, cap=None, split=False):
     assert ost == 0
     send, ros, boff, st = gpu_dispatch(x, topk, rank, g, plan, split=split)
     assert st == 0, st
-    assert np.array_equal(boff, oboff), "block_off"
-    assert np.array_equal(ros, oros), "row_of_slot"
-    assert np.array_equal(send, osend), "send"
+    assert_same(f"block_off rank {rank}", boff, oboff)
+    assert_same(f"row_of_slot rank {rank}", ros, oros)
+    assert_same(f"send rank {rank}", send, osend)
     if w is not None:
         cap = g.R * g.n_slot if cap is None else cap
         ostg, odoff, n_out, ost = oracle.pack(w, rank, og, op, cap)
         assert ost == 0
         stg, doff, st = gpu_pack(w, rank, g, plan, cap)
         assert st == 0, st
-        assert np.array_equal(doff, odoff), "dest_off"
-        assert np.array_equal(stg[:n_out], ostg[:n_out]), "staging"
+        assert_same(f"dest_off rank {rank}", doff, odoff)
+        assert_same(f"staging rank {rank}", stg[:n_out], ostg[:n_out])
         assert (stg[n_out:] == 0x3C3C).all(), "staging written past n_out"

@@ -17,6 +17,9 @@ if torch.cuda.is_available():
     import paper_2606_04101_amd as uep
 
 
+OUT_POISON = 0x7FA5  # a NaN payload: the combine writes every NaN as 0x7FC0
+
+
 class Pipe:
     """One workload's buffers and its calls, in order."""
 
@@ -54,7 +57,7 @@ class Pipe:
         self.src = torch.empty(max(c.R * c.n_slot, 1), dtype=torch.int32, device=dev)
         self.vol = torch.empty(c.R, dtype=torch.int32, device=dev)
         self.rst = torch.empty(4, dtype=torch.int64, device=dev)
-        self.out = torch.empty((T, H), dtype=torch.int16, device=dev)
+        self.out = torch.full((T, H), OUT_POISON, dtype=torch.int16, device=dev)
 
     def calls(self):
         c, g, p = self.c, self.g, self
@@ -71,28 +74,50 @@ class Pipe:
         ]
 
     def check(self):
-        c = self.c
-        assert int(self.st.item()) == 0
+        c, name = self.c, f"workload {self.c.cid} microbatch {self.m} rank {self.rank}"
+        assert int(self.st.item()) == 0, name
         ocnt, _ = oracle.count(self.tk_all, c.E, c.R)
-        assert np.array_equal(self.load.cpu().numpy(), ocnt)
+        gp.assert_same(f"{name} counts", self.load.cpu().numpy(), ocnt)
         gp.assert_plan_equal(self.plan, self.op)
         osend, oros, oboff, _ = oracle.dispatch(self.x_h, self.tk_all[self.rank], self.rank,
                                                 self.og, self.op)
-        assert np.array_equal(self.ros.cpu().numpy(), oros)
-        assert np.array_equal(self.boff.cpu().numpy(), oboff)
-        assert np.array_equal(gp.host_u16(self.send), osend)
+        gp.assert_same(f"{name} row_of_slot", self.ros.cpu().numpy(), oros)
+        gp.assert_same(f"{name} block_off", self.boff.cpu().numpy(), oboff)
+        gp.assert_same(f"{name} send", gp.host_u16(self.send), osend)
         ostg, odoff, n_out, _ = oracle.pack(self.w_h, self.rank, self.og, self.op, self.cap)
-        assert np.array_equal(self.doff.cpu().numpy(), odoff)
-        assert np.array_equal(gp.host_u16(self.stg)[:n_out], ostg[:n_out])
+        gp.assert_same(f"{name} dest_off", self.doff.cpu().numpy(), odoff)
+        gp.assert_same(f"{name} staging", gp.host_u16(self.stg)[:n_out], ostg[:n_out])
         rel = oracle.relay(self.og, self.op, 4)
-        assert np.array_equal(self.src.cpu().numpy()[: c.R * c.n_slot].reshape(c.R, c.n_slot),
-                              rel.slot_src.reshape(c.R, c.n_slot))
-        assert np.array_equal(self.vol.cpu().numpy(), rel.send_vol)
+        gp.assert_same(f"{name} slot_src",
+                       self.src.cpu().numpy()[: c.R * c.n_slot].reshape(c.R, c.n_slot),
+                       rel.slot_src.reshape(c.R, c.n_slot))
+        gp.assert_same(f"{name} send_vol", self.vol.cpu().numpy(), rel.send_vol)
         oout, _ = oracle.combine(osend, self.gate_h, oros)
-        assert np.array_equal(gp.host_u16(self.out), oout)
+        out = gp.host_u16(self.out)
+        if not np.array_equal(out, oout):
+            # facts that tell a kernel fault from a visibility fault, gathered
+            # once: elements never written (still the poison), a second read
+            # of the same buffer, and the combine run again alone on the
+            # default stream over the same inputs
+            bad = out != oout
+            poison = int((out[bad] == OUT_POISON).sum())
+            again = gp.host_u16(self.out)
+            fresh = torch.full_like(self.out, OUT_POISON)
+            st = gp.zero_status()
+            T, k, H = c.T, c.k, c.H
+            uep.ultraep_combine(self.send, T * k, self.gate, self.ros, T, k, H, fresh, st)
+            torch.cuda.synchronize()
+            rerun = gp.host_u16(fresh)
+            print(f"{name}: {int(bad.sum())} combine outputs differ, {poison} of them still "
+                  f"hold the poison; a second read differs from the first in "
+                  f"{int((again != out).sum())}; the combine run again alone differs from "
+                  f"the oracle in {int((rerun != oout).sum())} (status {int(st.item())})",
+                  flush=True)
+            gp.assert_same(f"{name} combine out", out, oout)
 
 
 def test_two_pipelines_on_two_streams():
+    print("two pipelines: workload 2 microbatch 0, workload 3 microbatch 4", flush=True)
     pipes = [Pipe(2, 0, 8 * 4096), Pipe(3, 4, 8 * 4096)]
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
     for s in streams:
@@ -104,5 +129,10 @@ def test_two_pipelines_on_two_streams():
                 with torch.cuda.stream(s):
                     f()
     torch.cuda.synchronize()
-    for p in pipes:
-        p.check()
+    errors = []
+    for p in pipes:  # both pipelines are checked before any failure is raised
+        try:
+            p.check()
+        except AssertionError as e:
+            errors.append(str(e))
+    assert not errors, "\n".join(errors)
