@@ -142,6 +142,26 @@ int ultraep_plan(const int32_t *load, const ultraep_group *g,
                  const ultraep_plan_buf *out, void *ws, size_t ws_bytes,
                  hipStream_t stream);
 
+/* ultraep_plan for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same kernels and outputs as ultraep_plan, with the planner workspace
+ * taken from a fixed array in the library's device memory instead of a
+ * caller buffer.  The array holds ULTRAEP_PLAN_STATIC_WS_BYTES (4.25 MiB),
+ * enough for every supported group (R <= 64, E <= 1024, R * n_slot <= 256);
+ * a group that would need more is rejected with ULTRAEP_EINVAL before any
+ * launch.  Each device the library runs on holds its own copy from the
+ * first call on that device (made with that device current) until the
+ * process ends.  The call allocates nothing and launches the planner's
+ * kernels only; the first kernel clears the part of the array that must
+ * start at zero.  Every call on one device shares that device's array:
+ * calls that overlap in time on one device (on different streams without
+ * an ordering between them, or from several host threads) race on it, so
+ * the caller serialises them.  ULTRAEP_EDEVICE if the array's device
+ * address cannot be obtained or a launch fails. */
+#define ULTRAEP_PLAN_STATIC_WS_BYTES ((size_t)17 << 18)
+int ultraep_plan_noalloc(const int32_t *load, const ultraep_group *g,
+                         const ultraep_plan_buf *out, hipStream_t stream);
+
 /* The two halves of ultraep_plan, in this order on one stream (or with the
  * second made to wait for the first): SolveReplication writes slot_expert,
  * quota, host_ptr, host_rank, host_pslot and stats; SolveReroute then writes

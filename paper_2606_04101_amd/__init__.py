@@ -81,6 +81,7 @@ def lib():
         L.ultraep_plan_sizes.argtypes = [gp, ctypes.POINTER(sz)]
         L.ultraep_count.argtypes = [_P, i64, i32, i32, i32, _P, _P, _P]
         L.ultraep_plan.argtypes = [_P, gp, pp, _P, sz, _P]
+        L.ultraep_plan_noalloc.argtypes = [_P, gp, pp, _P]
         L.ultraep_plan_replicate.argtypes = [_P, gp, pp, _P, sz, _P]
         L.ultraep_plan_reroute.argtypes = [_P, gp, pp, _P]
         L.ultraep_plan_ws_bytes.argtypes = [gp]
@@ -104,7 +105,7 @@ def lib():
         L.ultraep_strerror.argtypes = [ctypes.c_int]
         L.ultraep_strerror.restype = ctypes.c_char_p
         for f in ("ultraep_plan_sizes", "ultraep_count", "ultraep_plan",
-                  "ultraep_plan_replicate", "ultraep_plan_reroute",
+                  "ultraep_plan_noalloc", "ultraep_plan_replicate", "ultraep_plan_reroute",
                   "ultraep_dispatch", "ultraep_dispatch_layout",
                   "ultraep_dispatch_scatter", "ultraep_pack_replicas",
                   "ultraep_reroute_and_pack", "ultraep_relay_plan",
@@ -198,6 +199,15 @@ def ultraep_plan(load, g: Group, plan: Plan, ws=None, stream=None):
                                      ctypes.byref(plan.c), _ptr(ws),
                                      ws.numel() * ws.element_size(),
                                      _stream(stream)), "ultraep_plan")
+
+
+def ultraep_plan_noalloc(load, g: Group, plan: Plan, stream=None):
+    """ultraep_plan with the library's fixed per-device workspace (plan.ws is
+    not used); calls on one device must not overlap in time."""
+    _need(load, g.R * g.E, 4, "load")
+    return _check(lib().ultraep_plan_noalloc(_ptr(load), ctypes.byref(g),
+                                             ctypes.byref(plan.c), _stream(stream)),
+                  "ultraep_plan_noalloc")
 
 
 def ultraep_plan_replicate(load, g: Group, plan: Plan, ws=None, stream=None):

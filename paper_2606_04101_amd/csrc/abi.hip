@@ -1,12 +1,44 @@
 // C ABI of the UltraEP balancing library (see include/ultraep.h): argument
 // validation on the host, then stream-ordered kernel launches.  No
-// allocation, no host synchronisation, no memset.
+// allocation, no host synchronisation, no memset.  The one piece of library
+// state is the fixed planner workspace of ultraep_plan_noalloc.
 #include <stdint.h>
+
+#include <atomic>
+#include <mutex>
 
 #include "common.hpp"
 #include "kernels.hpp"
 
+// Planner workspace of ultraep_plan_noalloc: one copy per device, resident
+// for the life of the process.  Host code never uses this name as an
+// address: a device's copy is reached only through the pointer that
+// hipGetSymbolAddress returns for it.
+static __device__ __align__(256) uint8_t scratch[ULTRAEP_PLAN_STATIC_WS_BYTES];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of the current device's copy of `scratch`, looked up once
+// per device (nullptr on failure).
+void *scratch_of_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    void *q = nullptr;
+    if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return nullptr;
+    g_scratch_ptr[dev].store(q, std::memory_order_release);
+    p = q;
+  }
+  return p;
+}
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -84,6 +116,16 @@ int ultraep_plan(const int32_t *load, const ultraep_group *g,
                  hipStream_t stream) {
   if (!load || !group_ok(g) || !plan_ok(g, out) || !ws) return ULTRAEP_EINVAL;
   if (ws_bytes < uep::plan_ws_bytes(g->R, g->E, g->n_slot)) return ULTRAEP_EINVAL;
+  return rc(uep::launch_plan(load, *g, *out, ws, stream));
+}
+
+int ultraep_plan_noalloc(const int32_t *load, const ultraep_group *g,
+                         const ultraep_plan_buf *out, hipStream_t stream) {
+  if (!load || !group_ok(g) || !plan_ok(g, out)) return ULTRAEP_EINVAL;
+  if (uep::plan_ws_bytes(g->R, g->E, g->n_slot) > ULTRAEP_PLAN_STATIC_WS_BYTES)
+    return ULTRAEP_EINVAL;
+  void *ws = scratch_of_current_device();
+  if (!ws) return ULTRAEP_EDEVICE;
   return rc(uep::launch_plan(load, *g, *out, ws, stream));
 }
 

@@ -53,6 +53,18 @@ def test_plan_ws_bytes():
     assert uep.ultraep_plan_ws_bytes(uep.Group(3, 8, 1, 1)) == 0
 
 
+def test_noalloc_planner_array_covers_every_supported_group():
+    """The fixed workspace of ultraep_plan_noalloc holds the planner
+    workspace of the largest supported group."""
+    m = re.search(r"#define ULTRAEP_PLAN_STATIC_WS_BYTES \(\(size_t\)(\d+) << (\d+)\)",
+                  open(HEADER).read())
+    cap = int(m.group(1)) << int(m.group(2))
+    worst = max(uep.ultraep_plan_ws_bytes(uep.Group(R, E, ns, 1))
+                for R, E, ns in [(64, 1024, 4), (64, 64, 4), (32, 1024, 8), (16, 1024, 16),
+                                 (1, 1024, 256), (2, 1024, 128)])
+    assert 0 < worst <= cap < worst + (1 << 20)
+
+
 def test_ws_bytes():
     g = uep.Group(64, 256, 1, 1024)
     n = uep.ultraep_dispatch_ws_bytes(4096, 8, g)
