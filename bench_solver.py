@@ -37,6 +37,20 @@ GRID_NS = (1, 2, 4)               # redundant slots per rank
 GRID_ALPHA = (0.2, 0.35, 0.5)     # Zipf exponent of the router bias
 
 
+def sweep_configs(tokens=8192, quick=False):
+    """The grid's settings in order, as seeded generator configurations."""
+    import gen
+    sid = 0
+    for E, k in GRID_MOE:
+        for R in (GRID_R if not quick else (64,)):
+            for NS in GRID_NS:
+                for alpha in (GRID_ALPHA if not quick else (0.35,)):
+                    sid += 1
+                    yield gen.Config(200 + sid, f"sweep{sid}", R=R, E=E, n_slot=NS, k=k,
+                                     T=tokens, H=8, F=8, u_min=1024, bias="zipf", zipf_s=1.0,
+                                     bias_scale=alpha)
+
+
 def metrics(load, U, host_ptr, host_rank, Q):
     """Table 3 metrics of one plan (host numpy arrays: load [R][E], U [E][R],
     host_ptr [E+1], host_rank [ncol], Q [R][ncol])."""
@@ -90,52 +104,45 @@ def main():
     st = torch.zeros(1, dtype=torch.int32, device=dev)
     rows = []
     t0 = time.time()
-    sid = 0
-    for E, k in GRID_MOE:
-        for R in (GRID_R if not args.quick else (64,)):
-            for NS in GRID_NS:
-                for alpha in (GRID_ALPHA if not args.quick else (0.35,)):
-                    sid += 1
-                    c = gen.Config(200 + sid, f"sweep{sid}", R=R, E=E, n_slot=NS, k=k, T=args.tokens,
-                                   H=8, F=8, u_min=1024, bias="zipf", zipf_s=1.0,
-                                   bias_scale=alpha)
-                    tk = torch.from_numpy(gen.topk_all(c, 0)).to(dev)
-                    g = uep.Group(R, E, NS, c.u_min, c.beta_num, c.beta_den)
-                    load = torch.empty((R, E), dtype=torch.int32, device=dev)
-                    uep.ultraep_count(tk, c.T, k, E, R, load, st)
-                    plan = uep.Plan(g, dev)
-                    fn = lambda: uep.ultraep_plan(load, g, plan)
-                    fn()
-                    torch.cuda.synchronize()
-                    gr = torch.cuda.CUDAGraph()
-                    with torch.cuda.graph(gr):
-                        for _ in range(20):
-                            fn()
-                    gr.replay()
-                    torch.cuda.synchronize()
-                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    ts = []
-                    for _ in range(5):
-                        e0.record()
-                        gr.replay()
-                        e1.record()
-                        torch.cuda.synchronize()
-                        ts.append(1e3 * e0.elapsed_time(e1) / 20)
-                    assert int(st.item()) == 0 and int(plan.stats[6].item()) == 0
-                    ncol = g.ncol
-                    m = metrics(load.cpu().numpy(), plan.quota.cpu().numpy().reshape(E, R),
-                                plan.host_ptr.cpu().numpy(), plan.host_rank.cpu().numpy(),
-                                plan.reroute.cpu().numpy().reshape(R, ncol).astype(np.int64))
-                    m.update({"E": E, "k": k, "R": R, "n_slot": NS, "alpha": alpha,
-                              "tau_star": int(plan.stats[0].item()),
-                              "probes": int(plan.stats[3].item()),
-                              "solve_us": round(float(np.median(ts)), 2)})
-                    rows.append(m)
-                    print(f"# E={E} R={R} n_slot={NS} alpha={alpha}: before {m['imbalance_before']:.2f} "
-                          f"after {m['imbalance_after']:.3f} replicas {m['replicas']} max|H| {m['max_hosts']} "
-                          f"inflight {m['inflight']:.3f}/{m['inflight_no_locality']:.3f} "
-                          f"solve {m['solve_us']} us", file=sys.stderr, flush=True)
-                    del gr, plan, load, tk
+    for c in sweep_configs(args.tokens, args.quick):
+        E, k, R, NS, alpha = c.E, c.k, c.R, c.n_slot, c.bias_scale
+        tk = torch.from_numpy(gen.topk_all(c, 0)).to(dev)
+        g = uep.Group(R, E, NS, c.u_min, c.beta_num, c.beta_den)
+        load = torch.empty((R, E), dtype=torch.int32, device=dev)
+        uep.ultraep_count(tk, c.T, k, E, R, load, st)
+        plan = uep.Plan(g, dev)
+        fn = lambda: uep.ultraep_plan(load, g, plan)
+        fn()
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for _ in range(20):
+                fn()
+        gr.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ts = []
+        for _ in range(5):
+            e0.record()
+            gr.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(1e3 * e0.elapsed_time(e1) / 20)
+        assert int(st.item()) == 0 and int(plan.stats[6].item()) == 0
+        ncol = g.ncol
+        m = metrics(load.cpu().numpy(), plan.quota.cpu().numpy().reshape(E, R),
+                    plan.host_ptr.cpu().numpy(), plan.host_rank.cpu().numpy(),
+                    plan.reroute.cpu().numpy().reshape(R, ncol).astype(np.int64))
+        m.update({"E": E, "k": k, "R": R, "n_slot": NS, "alpha": alpha,
+                  "tau_star": int(plan.stats[0].item()),
+                  "probes": int(plan.stats[3].item()),
+                  "solve_us": round(float(np.median(ts)), 2)})
+        rows.append(m)
+        print(f"# E={E} R={R} n_slot={NS} alpha={alpha}: before {m['imbalance_before']:.2f} "
+              f"after {m['imbalance_after']:.3f} replicas {m['replicas']} max|H| {m['max_hosts']} "
+              f"inflight {m['inflight']:.3f}/{m['inflight_no_locality']:.3f} "
+              f"solve {m['solve_us']} us", file=sys.stderr, flush=True)
+        del gr, plan, load, tk
     keys = ("imbalance_before", "imbalance_after", "replicas", "sum_hosts", "max_hosts", "inflight",
             "inflight_no_locality", "solve_us")
     avg = {kk: round(float(np.mean([r[kk] for r in rows])), 4) for kk in keys}

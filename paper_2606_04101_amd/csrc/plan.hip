@@ -676,97 +676,96 @@ __device__ __forceinline__ int split_two(int lamhat, int Dr, int u0_init, int R)
   return qout;
 }
 
-// 1 if a < b, for |a - b| < 2^31: the sign of the difference, no compare
-__device__ __forceinline__ int lt01(int a, int b) {
-  return static_cast<int>(static_cast<uint32_t>(a - b) >> 31);
+// LDS of one expert's SolveReroute: its hosts' ranks (kWave), then the
+// shares of the lane-mirrored split (8 hosts x kMaxR sources, and a spare
+// area for the lanes that are not host slots)
+constexpr int kRrLds = kWave + 8 * kMaxR + kWave;
+
+// DPP row_ror:k - within each row of 16 lanes, a rotation by k lanes (the
+// 0 for `old` lets the compiler fold the move into the consuming add)
+template <int K>
+__device__ __forceinline__ int row_ror(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x120 + K, 0xF, 0xF, false);
 }
 
-// A few hosts (NH of them, home first): the same chain as split_two with
-// the residual quotas of hosts 0 .. NH-2 carried from lane r to lane r + 1;
-// the last host's quota is the rest of the residual demand.  Each source
-// computes the floor and remainder of lh * u_i / D for those hosts side by
-// side; for the last host they follow from the sum S of the others'
-// remainders, since all remainders add up to (leftover units) * D:
-// leftover = ceil(S / D) and its remainder is leftover * D - S.  The
-// leftover units go to the largest remainders (ties to the earlier host).
-// Needs lh * u below 2^52 (total load below 2^26).  Lane r returns source
-// r's share for each host in q[].
-template <int NH>
-__device__ __forceinline__ void split_small(int lamhat, int Dr, int (&u)[NH], int R, int (&q)[NH]) {
-  const bool act = lamhat > 0;
-  const double lhd = static_cast<double>(lamhat);
-  const int Di = act ? Dr : 1;
-  const double rD = 1.0 / static_cast<double>(Di);
-  const int lane = lane_id();
-#pragma unroll
-  for (int i = 0; i < NH; ++i) q[i] = 0;
-  for (int r = 0; r < R; ++r) {
-    int b[NH], rem[NH];
-    int sb = 0, srem = 0;
-#pragma unroll
-    for (int i = 0; i < NH - 1; ++i) {
-      // floor(lh * u / D) within one from the fp64 estimate (the product
-      // is exact); the remainder for that estimate lies in (-D, 2D), so
-      // wrapping 32-bit arithmetic gives it exactly
-      const int bi = static_cast<int>(lhd * static_cast<double>(u[i]) * rD);
-      const int ri = static_cast<int>(static_cast<uint32_t>(lamhat) * static_cast<uint32_t>(u[i]) -
-                                      static_cast<uint32_t>(bi) * static_cast<uint32_t>(Di));
-      const int lo = lt01(ri, 0), hi = 1 - lt01(ri, Di);
-      b[i] = bi + hi - lo;
-      rem[i] = ri + (lo - hi) * Di;
-      sb += b[i];
-      srem += rem[i];
-    }
-    // srem < (NH - 1) * D: leftover = ceil(srem / D), at most NH - 1
-    int left = 0;
-#pragma unroll
-    for (int k = 1; k < NH; ++k) left += lt01((k - 1) * Di, srem);
-    rem[NH - 1] = left * Di - srem;
-    b[NH - 1] = lamhat - sb - left;
-    const bool me = lane == r;
-#pragma unroll
-    for (int i = 0; i < NH; ++i) {
-      int rk = 0;  // hosts ahead of i in (remainder descending, host ascending)
-#pragma unroll
-      for (int k = 0; k < NH; ++k)
-        if (k != i) rk += k < i ? 1 - lt01(rem[k], rem[i]) : lt01(rem[i], rem[k]);
-      const int qi = b[i] + lt01(rk, left);
-      q[i] = me ? qi : q[i];
-      if (i < NH - 1) u[i] = wave_shr1(u[i] - qi);
-    }
-  }
+// 1 when the host k rotations away has the larger key (its key minus ours
+// is positive; keys are below 2^29, so the difference cannot wrap)
+template <int K>
+__device__ __forceinline__ int ahead(int key) {
+  return static_cast<int>(static_cast<uint32_t>(key - row_ror<K>(key)) >> 31);
 }
 
-// Runs split_small for NH hosts: hosts' ranks t[] and residual quotas come
-// from the replica mask; writes rows of Q (lane = source rank).
-template <int NH>
-__device__ __forceinline__ void reroute_small(int h, uint64_t rep, int lamhat_r, int Dr, int ures_r,
-                              int loc_r, int R, int32_t *qrow, int j0) {
-  const int lane = lane_id();
-  int t[NH], u[NH], q[NH];
-  t[0] = h;
-  uint64_t mrest = rep;
-#pragma unroll
-  for (int i = 1; i < NH; ++i) {
-    t[i] = __ffsll(static_cast<unsigned long long>(mrest)) - 1;
-    mrest &= mrest - 1;
+// Three to eight hosts, total load below 2^26: host i sits in lane i and in
+// its mirror lane i + 8, so that rotations by 1 .. 7 within the 16 lanes of
+// row 0 bring every other host's value to every host lane with no scalar
+// round trip.  Lanes of host slots i >= nh, and every lane past 15, hold a
+// zero residual quota (so a zero share and a zero remainder).  Per source
+// with residual demand, in ascending order:
+//   b_i = floor(lh * u_i / D) and rem_i exactly: the estimate
+//         trunc((lh / D) * u_i) in fp64 is within one of the floor (the
+//         quotient is below 2^26), and the remainder for the estimate lies
+//         in (-D, 2D), so wrapping 32-bit arithmetic gives it exactly and
+//         one correction gives both,
+//   left = lh - sum_i b_i, the sum taken by three rotations (4, 2, 1),
+//   host i gets one of the left units iff fewer than `left` hosts are ahead
+//   of it in (remainder descending, host ascending): the keys rem * 8 +
+//   (7 - i) order exactly so, and a zero-quota slot i >= nh is never ahead
+//   of a host (its key 7 - i is below every host's),
+// then u_i -= q_i.  The shares go to s_q[r * 8 + i] (lanes past 7 write a
+// spare area); afterwards lane r writes source r's row of Q, adding the
+// locality share of the host that is r itself.  s_hosts lists the hosts'
+// ranks, s_q holds kRrLds - kWave ints.
+__device__ __forceinline__ void split_lanes8(int lane, int nh, int lamhat_r, int Dr, int loc_r,
+                                             int R, int64_t ncol, int32_t *qbase,
+                                             const int32_t *s_hosts, int32_t *s_q,
+                                             int ures_r) {
+  const int hidx = lane & 7;
+  const bool slot = lane < 16 && hidx < nh;
+  int ures = __shfl(ures_r, slot ? s_hosts[hidx] : 0);
+  ures = slot ? ures : 0;
+  // lh / D of source `lane`
+  const double c_r = lamhat_r > 0 ? static_cast<double>(lamhat_r) / static_cast<double>(Dr) : 0.0;
+  const int qstep = lane < 8 ? 8 : 0;
+  const int qoff = lane < 8 ? lane : 8 * kMaxR + lane;
+  uint64_t act = ballot(lane < R && lamhat_r > 0);
+  const int key_lo = 7 - hidx;
+  while (act) {
+    const int r = __ffsll(static_cast<unsigned long long>(act)) - 1;
+    act &= act - 1;
+    const int lh = readlane(lamhat_r, r);
+    const int D = readlane(Dr, r);
+    const double c = readlane_d(c_r, r);
+    const int be = static_cast<int>(c * static_cast<double>(ures));
+    const int re = static_cast<int>(static_cast<uint32_t>(lh) * static_cast<uint32_t>(ures) -
+                                    static_cast<uint32_t>(be) * static_cast<uint32_t>(D));
+    const bool lo = re < 0, hi = re >= D;
+    const int b = lo ? be - 1 : (hi ? be + 1 : be);
+    const int rem = lo ? re + D : (hi ? re - D : re);
+    int sb = b + row_ror<4>(b);
+    sb += row_ror<2>(sb);
+    sb += row_ror<1>(sb);
+    const int left = lh - sb;
+    const int key = rem * 8 + key_lo;
+    const int rk = (ahead<1>(key) + ahead<2>(key)) + (ahead<3>(key) + ahead<4>(key)) +
+                   ((ahead<5>(key) + ahead<6>(key)) + ahead<7>(key));
+    const int qi = b + ((slot && rk < left) ? 1 : 0);
+    ures -= qi;
+    s_q[r * qstep + qoff] = qi;
   }
-#pragma unroll
-  for (int i = 0; i < NH; ++i) u[i] = readlane(ures_r, t[i]);
-  split_small<NH>(lamhat_r, Dr, u, R, q);
   if (lane < R) {
-#pragma unroll
-    for (int i = 0; i < NH; ++i) qrow[j0 + i] = q[i] + (lane == t[i] ? loc_r : 0);
+    const bool dem = lamhat_r > 0;
+    int32_t *qrow = qbase + static_cast<int64_t>(lane) * ncol;
+    for (int i = 0; i < nh; ++i)
+      qrow[i] = (dem ? s_q[lane * 8 + i] : 0) + (s_hosts[i] == lane ? loc_r : 0);
   }
 }
 
 // Any number of hosts: lane i is host i (home first, then replicas by
 // ascending rank) with residual quota ures; the sources run in ascending
 // order, each splitting its residual demand by largest remainder.  Writes
-// q of source r, host `lane` to qcol[r * ncol].  kNH > 0: exactly kNH
-// hosts, the remainder ranking unrolled over lanes 0 .. kNH-1 with no
-// branch.
-template <bool kExact, bool kOneRow, int kNH>
+// q of source r, host `lane` to qcol[r * ncol].  Used above eight hosts or
+// when the total load reaches 2^26.
+template <bool kExact, bool kOneRow>
 __device__ __forceinline__ void split_many(int lane, int nh, int lamhat_r, int Dr, int ures, int R,
                            int64_t ncol, int32_t *qcol, int t_i, int qloc_i) {
   const double rDr = lamhat_r > 0 ? 1.0 / static_cast<double>(Dr) : 0.0;
@@ -798,17 +797,9 @@ __device__ __forceinline__ void split_many(int lane, int nh, int lamhat_r, int D
       const int left = lh - (kOneRow ? readlane(row_sum(b), 0) : wave_sum(b));
       // the `left` hosts with the largest remainders (ties: earlier host)
       int rk = 0;
-      if (kNH > 0) {
-#pragma unroll
-        for (int j = 0; j < kNH; ++j) {
-          const int rj = readlane(rem, j);
-          rk += (rj > rem) || (rj == rem && j < lane);
-        }
-      } else {
-        for (int j = 0; j < nh; ++j) {
-          const int rj = readlane(rem, j);
-          rk += (rj > rem) || (rj == rem && j < lane);
-        }
+      for (int j = 0; j < nh; ++j) {
+        const int rj = readlane(rem, j);
+        rk += (rj > rem) || (rj == rem && j < lane);
       }
       qi = b + ((host && rk < left) ? 1 : 0);
       ures -= qi;
@@ -860,14 +851,16 @@ __device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0,
       qrow[j0] = q0 + (lane == h ? loc_r : 0);
       qrow[j0 + 1] = lamhat_r - q0 + (lane == t ? loc_r : 0);
     }
-  } else if (exact && nh == 3) {
-    reroute_small<3>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
-  } else if (exact && nh == 4) {
-    reroute_small<4>(h, rep, lamhat_r, Dr, ures_r, loc_r, R, qrow, j0);
   } else {
     if (lane == h) s_t[0] = h;
     if ((rep >> lane) & 1) s_t[1 + popc_below(rep)] = lane;
     __syncthreads();
+    if (exact && nh <= 8) {
+      split_lanes8(lane, nh, lamhat_r, Dr, loc_r, R, ncol, a.q + j0, s_t, s_t + kWave, ures_r);
+      for (int j = total + e; j < ncol; j += E)
+        if (lane < R) qrow[j] = 0;
+      return;
+    }
     const int t_i = lane < nh ? s_t[lane] : 0;
     // every lane takes part in the shuffles: a lane reads only from lanes
     // that execute the same shuffle
@@ -875,22 +868,14 @@ __device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0,
     const int qloc_i = __shfl(loc_r, t_i);
     const int ures_i = lane < nh ? ures_t : 0;
     int32_t *qcol = a.q + j0 + lane;
-    if (exact && nh == 5)
-      split_many<true, true, 5>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-    else if (exact && nh == 6)
-      split_many<true, true, 6>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-    else if (exact && nh == 7)
-      split_many<true, true, 7>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-    else if (exact && nh == 8)
-      split_many<true, true, 8>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
-    else if (exact && nh <= 16)
-      split_many<true, true, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+    if (exact && nh <= 16)
+      split_many<true, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
     else if (exact)
-      split_many<true, false, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+      split_many<true, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
     else if (nh <= 16)
-      split_many<false, true, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+      split_many<false, true>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
     else
-      split_many<false, false, 0>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
+      split_many<false, false>(lane, nh, lamhat_r, Dr, ures_i, R, ncol, qcol, t_i, qloc_i);
   }
   // CSR padding columns of Q
   for (int j = total + e; j < ncol; j += E)
@@ -903,7 +888,7 @@ __device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0,
 // the values it has just produced (ultraep_plan's single-launch ending).
 template <bool kReroute>
 __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
-  __shared__ int32_t s_t[kWave];
+  __shared__ int32_t s_t[kRrLds];
   __shared__ uint32_t s_et[kMaxRec];
   __shared__ int32_t s_d[kMaxRec];
   __shared__ int32_t s_ht[kMaxR];  // hosts of this expert: rank
@@ -1066,7 +1051,7 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
 }
 
 __global__ void __launch_bounds__(kWave) k_plan_reroute(PlanArgs a) {
-  __shared__ int32_t s_t[kWave];
+  __shared__ int32_t s_t[kRrLds];
   const int e = blockIdx.x, lane = threadIdx.x;
   const int R = a.R, E = a.E;
   const int64_t status = a.stats[6], L = a.stats[7];
@@ -1084,7 +1069,7 @@ __global__ void __launch_bounds__(kWave) k_plan_reroute(PlanArgs a) {
 // workgroups come first so they are placed before the packing fills the
 // chip.
 __global__ void __launch_bounds__(kPkThreads) k_reroute_pack(PlanArgs a, PkArgs p) {
-  __shared__ int32_t s_t[kWave];
+  __shared__ int32_t s_t[kRrLds];
   const int b = blockIdx.x;
   if (b < a.E) {
     if (threadIdx.x >= kWave) return;
