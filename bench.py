@@ -570,6 +570,8 @@ def per_workload(args):
             ts.append(1e3 * e0.elapsed_time(e1) / n)
         return round(float(np.median(ts)), 2)
 
+    gap = quality_gap_table()
+
     def instance(c, m, g, xw, n_cold):
         """One microbatch / layer m of workload c; xw holds the activations and
         weights (host and device) of the first instance's measured rank."""
@@ -613,6 +615,18 @@ def per_workload(args):
         rec["replicate_us"] = graph_us([lambda: uep.ultraep_plan_replicate(load, g, plan)])
         rec["reroute_us"] = graph_us([lambda: uep.ultraep_plan_reroute(load, g, plan)])
         rec["max_hosts"] = int(plan.stats[5].item())
+        # balancing quality: the bisection's threshold and the max rank load
+        # of its plan over the mean, next to the smallest greedy-feasible
+        # threshold of the stored table (written by the oracle-only script
+        # tests/golden/quality_gap.py)
+        Uq = plan.quota.cpu().numpy().reshape(c.E, c.R).astype(np.int64)
+        mean_load = float(Uq.sum()) / c.R
+        rec["tau_star"] = int(plan.stats[0].item())
+        rec["imbalance_after"] = round(float(Uq.sum(0).max()) / mean_load, 4) if mean_load else 1.0
+        row = gap.get(("w", c.cid, m))
+        if row:
+            rec["tau_min_feasible"] = row["tau_min"]
+            rec["imbalance_at_tau_min"] = row["imbalance_min"]
         rec["dispatch_us"] = cold_us(disp_f, n_cold)
         rec["scatter_us"] = cold_us(scat_f, n_cold)
         rec["pack_us"] = cold_us(pack_f, n_cold) if outb[rank] else None
@@ -670,10 +684,13 @@ def per_workload(args):
                                "scatter_us": med("scatter_us", "median"),
                                "pack_us": round(float(np.median([r["pack_us"]["median"] for r in recs
                                                                  if r["pack_us"]])), 2),
-                               "scatter_GBps": med("scatter_GBps")},
+                               "scatter_GBps": med("scatter_GBps"),
+                               "imbalance_after": med("imbalance_after")},
                     "max": {"count_plan_us": max(r["count_plan_us"] for r in recs),
                             "max_hosts": max(r["max_hosts"] for r in recs)},
                     "bit_exact_all": all(r["bit_exact"] for r in recs)}
+            if all("imbalance_at_tau_min" in r for r in recs):
+                summ["median"]["imbalance_at_tau_min"] = med("imbalance_at_tau_min")
             if cid == 5:
                 # count + plan of every layer back to back: one graph, 58 pairs
                 st = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -688,6 +705,20 @@ def per_workload(args):
             print(json.dumps({"summary": summ}), flush=True)
         del xw, recs, keep
         torch.cuda.empty_cache()
+
+
+def quality_gap_table():
+    """Rows of tests/golden/quality_gap.json keyed by ("w", workload,
+    instance) and ("s", E, R, n_slot, alpha, tokens); empty if absent."""
+    path = os.path.join(ROOT, "tests", "golden", "quality_gap.json")
+    if not os.path.exists(path):
+        return {}
+    with open(path) as f:
+        doc = json.load(f)
+    out = {("w", r["workload"], r["instance"]): r for r in doc["workloads"]}
+    out.update({("s", r["E"], r["R"], r["n_slot"], r["alpha"], r["tokens"]): r
+                for r in doc["sweep"]})
+    return out
 
 
 def oracle_baseline(c, tk_all, rank, x_h, w_h, cap):

@@ -19,6 +19,11 @@ popularity), counts it and plans it on the GPU, then reads the plan back:
                              1 - sum_t lambda_{t,e} u_{e,t} / lambda_e, per token
   solve_us                   ultraep_plan device latency: one call of a graph
                              of 20 consecutive calls
+  tau_min_feasible,          the smallest threshold whose greedy probe is
+  imbalance_at_tau_min       feasible (a linear scan; Algorithm 1's bisection
+                             can stop above it because feasibility is not
+                             monotone) and that probe's max rank load over
+                             the mean, from tests/golden/quality_gap.json
 Prints one JSON line: every setting and the averages.  Needs an MI355X."""
 from __future__ import annotations
 
@@ -102,6 +107,10 @@ def main():
 
     dev = torch.device("cuda:0")
     st = torch.zeros(1, dtype=torch.int32, device=dev)
+    # the smallest greedy-feasible threshold of each setting, from the table
+    # the oracle-only script tests/golden/quality_gap.py writes
+    from bench import quality_gap_table
+    gap = quality_gap_table()
     rows = []
     t0 = time.time()
     for c in sweep_configs(args.tokens, args.quick):
@@ -137,6 +146,11 @@ def main():
                   "tau_star": int(plan.stats[0].item()),
                   "probes": int(plan.stats[3].item()),
                   "solve_us": round(float(np.median(ts)), 2)})
+        q = gap.get(("s", E, R, NS, alpha, c.T))
+        if q:
+            assert q["tau_star"] == m["tau_star"], "stored table is of other loads"
+            m["tau_min_feasible"] = q["tau_min"]
+            m["imbalance_at_tau_min"] = q["imbalance_min"]
         rows.append(m)
         print(f"# E={E} R={R} n_slot={NS} alpha={alpha}: before {m['imbalance_before']:.2f} "
               f"after {m['imbalance_after']:.3f} replicas {m['replicas']} max|H| {m['max_hosts']} "
@@ -145,6 +159,8 @@ def main():
         del gr, plan, load, tk
     keys = ("imbalance_before", "imbalance_after", "replicas", "sum_hosts", "max_hosts", "inflight",
             "inflight_no_locality", "solve_us")
+    if all("imbalance_at_tau_min" in r for r in rows):
+        keys = keys + ("imbalance_at_tau_min",)
     avg = {kk: round(float(np.mean([r[kk] for r in rows])), 4) for kk in keys}
     print(json.dumps({"metric": "solver quality over a grid of synthetic power-law loads (Table 3 metrics)",
                       "settings": len(rows), "tokens_per_rank": args.tokens, "average": avg,

@@ -10,8 +10,11 @@
 // and every count is written (no global atomics, no zero-fill).
 // Larger blocks: one workgroup's LDS atomics become the limit (hot experts
 // make the lanes of an atomic collide), so a fill kernel zeroes the counts
-// and a grid of 256-thread workgroups, each counting 4096 ids into per-wave
-// LDS histograms, adds its non-zero bins with global atomics.
+// and a grid of 256-thread workgroups, each counting 2048 or 4096 ids into
+// per-wave LDS histograms, adds its non-zero bins with global atomics.
+// (Aggregating equal ids within a wave first, with bit-sliced ballot
+// matches and one LDS add per distinct id, measured five times slower: the
+// ballots cost far more than the collisions they save.)
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -71,10 +74,15 @@ k_count(const int32_t *__restrict__ topk, int64_t V, int32_t E,
   }
 }
 
-constexpr int64_t kSplitIds = 32768;
+// Above kSplitIds ids per block the split path runs; its workgroups take
+// 2048 ids each up to kSplitSmall ids per block, 4096 above (measured on one
+// rank's block of the workloads here: 32768 ids count in 4.1 us split
+// against 5.6 us in one workgroup, 131072 ids in 4.8 us with 4096 per
+// workgroup against 5.0 us with 2048).
+constexpr int64_t kSplitIds = 16384;
+constexpr int64_t kSplitSmall = 65536;
 constexpr int kSplitThreads = 256;
 constexpr int kSplitWaves = kSplitThreads / kWave;
-constexpr int kSplitPerWg = kSplitThreads * 16;  // ids per workgroup
 
 __global__ void __launch_bounds__(kSplitThreads)
 k_count_zero(int32_t *__restrict__ counts, int64_t n) {
@@ -82,10 +90,12 @@ k_count_zero(int32_t *__restrict__ counts, int64_t n) {
   if (i < n) counts[i] = 0;
 }
 
-// blockIdx.y = block of ids, blockIdx.x = its 4096-id part
+// blockIdx.y = block of ids, blockIdx.x = its part of kPerWg ids
+template <int kPerWg>
 __global__ void __launch_bounds__(kSplitThreads)
 k_count_split(const int32_t *__restrict__ topk, int64_t V, int32_t E,
               int32_t *__restrict__ counts, int32_t *status) {
+  constexpr int kSplitPerWg = kPerWg;
   extern __shared__ int32_t hist[];  // [kSplitWaves][E]
   const int wave = threadIdx.x / kWave;
   for (int i = threadIdx.x; i < kSplitWaves * E; i += kSplitThreads) hist[i] = 0;
@@ -139,9 +149,18 @@ hipError_t launch_count(const int32_t *topk, int64_t T, int32_t k, int32_t E,
   const int64_t n = static_cast<int64_t>(n_groups) * E;
   hipLaunchKernelGGL(k_count_zero, dim3(static_cast<unsigned>((n + kSplitThreads - 1) / kSplitThreads)),
                      dim3(kSplitThreads), 0, stream, counts, n);
-  const unsigned parts = static_cast<unsigned>((V + kSplitPerWg - 1) / kSplitPerWg);
-  hipLaunchKernelGGL(k_count_split, dim3(parts, n_groups), dim3(kSplitThreads),
-                     sizeof(int32_t) * kSplitWaves * E, stream, topk, V, E, counts, status);
+  const size_t lds = sizeof(int32_t) * kSplitWaves * E;
+  if (V <= kSplitSmall) {
+    constexpr int per = kSplitThreads * 8;
+    const unsigned parts = static_cast<unsigned>((V + per - 1) / per);
+    hipLaunchKernelGGL(k_count_split<per>, dim3(parts, n_groups), dim3(kSplitThreads), lds, stream,
+                       topk, V, E, counts, status);
+  } else {
+    constexpr int per = kSplitThreads * 16;
+    const unsigned parts = static_cast<unsigned>((V + per - 1) / per);
+    hipLaunchKernelGGL(k_count_split<per>, dim3(parts, n_groups), dim3(kSplitThreads), lds, stream,
+                       topk, V, E, counts, status);
+  }
   return hipGetLastError();
 }
 

@@ -681,11 +681,12 @@ __device__ __forceinline__ int split_two(int lamhat, int Dr, int u0_init, int R)
 // area for the lanes that are not host slots)
 constexpr int kRrLds = kWave + 8 * kMaxR + kWave;
 
-// DPP row_ror:k - within each row of 16 lanes, a rotation by k lanes (the
-// 0 for `old` lets the compiler fold the move into the consuming add)
+// DPP row_ror:k - within each row of 16 lanes, a rotation by k lanes (every
+// lane has a source, so no old value is needed and the move folds into the
+// instruction that consumes it)
 template <int K>
 __device__ __forceinline__ int row_ror(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, 0x120 + K, 0xF, 0xF, false);
+  return __builtin_amdgcn_mov_dpp(v, 0x120 + K, 0xF, 0xF, true);
 }
 
 // 1 when the host k rotations away has the larger key (its key minus ours
