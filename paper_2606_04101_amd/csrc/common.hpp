@@ -63,6 +63,20 @@ __device__ __forceinline__ int wave_sum(int v) {
                                         readlane(v, 32) + readlane(v, 48));
 }
 
+// Inclusive prefix sum over the 64 lanes: a Hillis-Steele scan inside each
+// row of 16 lanes with DPP row shifts (a lane without a source adds 0),
+// then each row adds the totals of the rows before it.  Every lane must be
+// active.
+__device__ __forceinline__ int wave_scan_incl(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  const int t0 = readlane(v, 15), t1 = readlane(v, 31), t2 = readlane(v, 47);
+  const int lane = lane_id();
+  return v + (lane >= 16 ? t0 : 0) + (lane >= 32 ? t1 : 0) + (lane >= 48 ? t2 : 0);
+}
+
 __device__ __forceinline__ int64_t wave_sum64(int64_t v) {
   int lo = static_cast<int>(static_cast<uint32_t>(v));
   int hi = static_cast<int>(v >> 32);

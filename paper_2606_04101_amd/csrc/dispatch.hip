@@ -118,11 +118,7 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_hist(DlArgs a) {
   // exclusive scan of cnt (two elements per thread) into int64 offsets
   const int b0 = 2 * tid, b1 = 2 * tid + 1;
   const int v0 = b0 < nblk ? cnt[b0] : 0, v1 = b1 < nblk ? cnt[b1] : 0;
-  int incl = v0 + v1;
-  for (int o = 1; o < kWave; o <<= 1) {
-    int t = __shfl_up(incl, o);
-    if (lane >= o) incl += t;
-  }
+  const int incl = wave_scan_incl(v0 + v1);
   if (lane == kWave - 1) tmp[wave] = incl;
   __syncthreads();
   if (tid == 0) {

@@ -832,11 +832,7 @@ __device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0,
   const int ures_r = u_r - loc_r;
   // residual demand still to place when source r comes: D0 minus the
   // demand of the sources before it
-  int incl = lamhat_r;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int t = __shfl_up(incl, o);
-    if (lane >= o) incl += t;
-  }
+  const int incl = wave_scan_incl(lamhat_r);
   const int D0 = readlane(incl, kWave - 1);
   const int Dr = D0 - (incl - lamhat_r);
   const bool exact = L < (int64_t(1) << 26);
