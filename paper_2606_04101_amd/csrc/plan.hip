@@ -261,16 +261,23 @@ __device__ __forceinline__ int wave_shl1(int v) {
 // descending load) with scalar loop state and a single exit.
 
 // Loads experts [j0, j0 + 64) of rank r's visiting order into lanes.
+// Lanes past the rank's last expert read that expert and hold zeros: no
+// divergent branch in the probes' loops.
 __device__ __forceinline__ void load_experts(const PlanArgs &a, int r, int j0, int lane,
                                              const int32_t *s_eorder, const int32_t *s_elam,
                                              int &ev, int &lv) {
   const int jl = j0 + lane;
-  ev = jl < a.nm ? s_eorder[r * a.nm + jl] : 0;
-  lv = jl < a.nm ? s_elam[r * a.nm + jl] : 0;
+  const int i = r * a.nm + min(jl, a.nm - 1);
+  const int v = s_eorder[i], l = s_elam[i];
+  ev = jl < a.nm ? v : 0;
+  lv = jl < a.nm ? l : 0;
 }
 
 // One redundant slot per rank: every transfer uses up its target, so
 // transfer k goes to the k-th listed target and its record stays in lane k.
+// The slacks never change, so P is the fixed inclusive prefix of the list
+// and the lanes with P - B < need are the prefix [0, hh) (lanes before the
+// head have P <= B): the whole targets are [h, hh).
 template <int kSite>
 __device__ __forceinline__ int probe_one_slot(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
                               int as_r, int as_l, const int32_t *s_eorder,
@@ -279,7 +286,6 @@ __device__ __forceinline__ int probe_one_slot(const PlanArgs &a, int tau, int la
   const bool tv = lane < R && as_l < tau;
   const int m = tv ? tau - as_l : 0;
   const uint64_t tmask = ballot(tv);  // a prefix of the lanes
-  const int nT = __popcll(tmask);
   // inclusive prefix of the slacks: each is below 2^25, the sum below 2^31
   int P = m;
   for (int o = 1; o < kWave; o <<= 1) {
@@ -298,36 +304,36 @@ __device__ __forceinline__ int probe_one_slot(const PlanArgs &a, int tau, int la
   for (;;) {
     const int c = readlane(lv, j & (kWave - 1));
     const int e = readlane(ev, j & (kWave - 1));
-    // an expert with no load left: the rank's excess cannot be shed
-    fail = c <= 0 || h >= nT;
-    if (fail) break;
     const int need = min(x, c);
-    const uint64_t whole = uni64(ballot(P - B < need) & tmask & (~uint64_t(0) << h));
-    const int hh = uni(h + __popcll(whole));
-    fail = (whole & low_umin) != 0 || hh >= nT;
-    if (fail) break;
-    const bool wl = (whole >> lane) & 1;
-    rec_e = wl ? e : rec_e;
-    rec_d = wl ? m : rec_d;
-    const int Ph = readlane(P, hh), mh = readlane(m, hh);
+    const uint64_t wm = ballot(P - B < need) & tmask;
+    const int hh = __popcll(wm);
+    const int Ph = readlane(P, hh & (kWave - 1)), mh = readlane(m, hh & (kWave - 1));
     const int taken = Ph - mh - B;  // slack of the whole targets
     const int d = need - taken;     // the rest, at most mh
     x -= taken;
-    const bool take = d >= u_min;
-    // d below u_min: infeasible unless only this expert's load is short
-    fail = !take && min(x, mh) < u_min;
+    const int take = d >= u_min ? 1 : 0;
+    // an expert with no load left, no target for the rest (every target
+    // whole), a whole target below u_min, or a rest below u_min that is not
+    // only this expert's shortfall (max(d, min(x, mh)) < u_min)
+    fail = c <= 0 || wm == tmask || ((wm & low_umin) >> (h & (kWave - 1))) != 0 ||
+           max(d, min(x, mh)) < u_min;
     if (fail) break;
-    rec_e = (take && lane == hh) ? e : rec_e;
-    rec_d = (take && lane == hh) ? d : rec_d;
+    // the whole targets and, when the rest is taken, target hh
+    const bool mine = static_cast<uint32_t>(lane - h) < static_cast<uint32_t>(hh - h + take);
+    rec_e = mine ? e : rec_e;
+    rec_d = mine ? (lane == hh ? d : m) : rec_d;
     x -= take ? d : 0;
-    B = uni(take ? Ph : Ph - mh);
-    h = uni(take ? hh + 1 : hh);
-    if (x > 0 && ++j < nm) {  // next expert of this rank
-      if ((j & (kWave - 1)) == 0) load_experts(a, r, j, lane, s_eorder, s_elam, ev, lv);
-      continue;
+    B = take ? Ph : Ph - mh;
+    h = hh + take;
+    if (x > 0) {
+      if (++j < nm) {  // next expert of this rank
+        if ((j & (kWave - 1)) == 0) load_experts(a, r, j, lane, s_eorder, s_elam, ev, lv);
+        continue;
+      }
+      fail = true;  // the rank's experts ran out
+      break;
     }
-    fail = x > 0;  // the rank's experts ran out
-    if (fail || ++oi >= R) break;
+    if (++oi >= R) break;
     x = readlane(rk_l, oi) - tau;
     if (x <= 0) break;  // the remaining ranks are not overloaded
     r = readlane(rk_r, oi);
@@ -345,7 +351,13 @@ __device__ __forceinline__ int probe_one_slot(const PlanArgs &a, int tau, int la
 // Several redundant slots per rank: a target that keeps slack and a free
 // slot after an expert's last (partial) transfer moves back to its place in
 // the list; the lanes it passes shift down by one (DPP) and P is patched.
-// The list entries are packed keys (slack << 6) | (63 - rank).
+// The list entries are packed keys (slack << 6) | (63 - rank).  P is
+// nondecreasing over the live lanes, and every lane before the head has
+// P <= B, so the lanes with P - B < need are the prefix [0, hh): hh is the
+// population count of one ballot, and the whole targets are [h, hh).  In
+// the loop a record is (e, key of the transfer: amount << 6 | 63 - rank),
+// written by the lanes of the targets themselves; the records are put into
+// the common (e | rank << 16, amount) form once the probe has succeeded.
 template <int kSite>
 __device__ __forceinline__ int probe_multi(const PlanArgs &a, int tau, int lane, int rk_r, int rk_l,
                            int as_r, int as_l, const int32_t *s_eorder,
@@ -355,12 +367,13 @@ __device__ __forceinline__ int probe_multi(const PlanArgs &a, int tau, int lane,
   int key = tv ? ((tau - as_l) << 6) | (kWave - 1 - as_r) : 0;
   int used = 0;
   const uint64_t live = ballot(tv);  // a prefix of the lanes; its length never changes
-  const int nT = __popcll(live);
   int P = key >> 6;
   for (int o = 1; o < kWave; o <<= 1) {
     const int t = __shfl_up(P, o);
     if (lane >= o) P += t;
   }
+  // live lanes whose slack is below u_min (refreshed when a key moves)
+  uint64_t low = ballot((key >> 6) < u_min);
   int x = readlane(rk_l, 0) - tau;
   if (x <= 0) return 0;
   int r = readlane(rk_r, 0);
@@ -371,65 +384,71 @@ __device__ __forceinline__ int probe_multi(const PlanArgs &a, int tau, int lane,
   for (;;) {
     const int c = readlane(lv, j & (kWave - 1));
     const int e = readlane(ev, j & (kWave - 1));
-    fail = c <= 0 || h >= nT;
-    if (fail) break;
     const int need = min(x, c);
-    const int m = key >> 6;
-    const uint64_t whole = uni64(ballot(P - B < need) & live & (~uint64_t(0) << h));
-    const uint64_t low = uni64(ballot(m < u_min));
-    const int hh = uni(h + __popcll(whole));
-    fail = (whole & low) != 0 || hh >= nT;
-    if (fail) break;
-    if ((whole >> lane) & 1) {
-      s_re[n + lane - h] = static_cast<uint32_t>(e) |
-                           (static_cast<uint32_t>(kWave - 1 - (key & (kWave - 1))) << 16);
-      s_rd[n + lane - h] = m;
-    }
-    n += hh - h;
-    const int Ph = readlane(P, hh), kh = readlane(key, hh);
+    const uint64_t wm = ballot(P - B < need) & live;
+    const int hh = __popcll(wm);
+    const int Ph = readlane(P, hh & (kWave - 1)), kh = readlane(key, hh & (kWave - 1));
     const int mh = kh >> 6;
-    const int taken = Ph - mh - B;
-    const int d = need - taken;
+    const int taken = Ph - mh - B;  // slack of the whole targets
+    const int d = need - taken;     // the rest, at most mh
     x -= taken;
-    const bool take = d >= u_min;
-    fail = !take && min(x, mh) < u_min;
+    const int take = d >= u_min ? 1 : 0;
+    // an expert with no load left, no target for the rest (every live lane
+    // whole), a whole target below u_min, or a rest below u_min that is not
+    // only this expert's shortfall (max(d, min(x, mh)) < u_min)
+    fail = c <= 0 || wm == live || ((wm & low) >> (h & (kWave - 1))) != 0 ||
+           max(d, min(x, mh)) < u_min;
     if (fail) break;
+    const int nw = hh - h + take;
+    {  // the other lanes write a spare area past the records
+      const int at = static_cast<uint32_t>(lane - h) < static_cast<uint32_t>(nw) ? n + lane - h
+                                                                             : kMaxRec + lane;
+      s_re[at] = static_cast<uint32_t>(e);
+      s_rd[at] = lane == hh ? ((d << 6) | (key & (kWave - 1))) : key;
+    }
+    n += nw;
     B = Ph - mh;
     h = hh;
     if (take) {
-      if (lane == 0) {
-        s_re[n] = static_cast<uint32_t>(e) | (static_cast<uint32_t>(kWave - 1 - (kh & (kWave - 1))) << 16);
-        s_rd[n] = d;
-      }
-      ++n;
       x -= d;
       const int uh = readlane(used, hh) + 1;
       if (mh == d || uh >= NS) {  // out of slack or slots: leaves the list
         B = Ph;
         h = hh + 1;
-      } else {  // back to its place: after every live key still larger
+      } else {  // back to its place: after every key still larger
         const int nk = ((mh - d) << 6) | (kh & (kWave - 1));
-        const int p = uni(hh + __popcll(ballot(lane > hh && key > nk) & live));
-        const bool mv = lane >= hh && lane < p;
+        const int p = hh + __popcll(ballot(key > nk) & (~uint64_t(1) << hh) & live);
+        const bool mv = static_cast<uint32_t>(lane - hh) < static_cast<uint32_t>(p - hh);
         const int ks = wave_shl1(key), us = wave_shl1(used), ps = wave_shl1(P);
         key = mv ? ks : (lane == p ? nk : key);
         used = mv ? us : (lane == p ? uh : used);
         P = mv ? ps - mh : (lane >= p ? P - d : P);
+        low = ballot((key >> 6) < u_min);
       }
     }
-    if (x > 0 && ++j < nm) {
-      if ((j & (kWave - 1)) == 0) load_experts(a, r, j, lane, s_eorder, s_elam, ev, lv);
-      continue;
+    if (x > 0) {
+      if (++j < nm) {  // next expert of this rank
+        if ((j & (kWave - 1)) == 0) load_experts(a, r, j, lane, s_eorder, s_elam, ev, lv);
+        continue;
+      }
+      fail = true;  // the rank's experts ran out
+      break;
     }
-    fail = x > 0;
-    if (fail || ++oi >= R) break;
+    if (++oi >= R) break;
     x = readlane(rk_l, oi) - tau;
-    if (x <= 0) break;
+    if (x <= 0) break;  // the remaining ranks are not overloaded
     r = readlane(rk_r, oi);
     load_experts(a, r, 0, lane, s_eorder, s_elam, ev, lv);
     j = 0;
   }
-  return fail ? -1 : n;
+  if (fail) return -1;
+  __syncthreads();
+  for (int i = lane; i < n; i += kWave) {
+    const int k = s_rd[i];
+    s_re[i] |= static_cast<uint32_t>(kWave - 1 - (k & (kWave - 1))) << 16;
+    s_rd[i] = k >> 6;
+  }
+  return n;
 }
 
 // The same probe for slacks of 25 bits or more: lane t holds rank t's slack
@@ -506,10 +525,12 @@ struct BisState {
   int probes; // probes of the sequential bisection so far
 };
 
+// One pointer and four loads whatever rd is (no branch that would make the
+// loads wait for each other).
 __device__ __forceinline__ BisState state_before(const PlanArgs &a, int rd) {
-  if (rd == 0) return {a.ws.hdr[0], a.ws.hdr[1], -1, 0};
-  const int64_t *h = a.ws.hdr + 4 + 4 * (rd - 1);
-  return {h[0], h[1], static_cast<int>(h[2]), static_cast<int>(h[3])};
+  const int64_t *h = a.ws.hdr + (rd == 0 ? 0 : 4 + 4 * (rd - 1));
+  const int64_t lo = h[0], hi = h[1], best = h[2], probes = h[3];
+  return {lo, hi, rd == 0 ? -1 : static_cast<int>(best), rd == 0 ? 0 : static_cast<int>(probes)};
 }
 
 __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
@@ -518,17 +539,21 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-// Round rd's outcome words, word w in lane w: the OR of its copies.
-__device__ __forceinline__ uint64_t outcome_words(const PlanArgs &a, int rd) {
-  const int lane = lane_id();
-  uint64_t v[kCopies];
+// Round rd's outcome words: the kCopies copies of word w into lane w (the
+// lanes past the last word read it too).  No branch between the loads, so
+// that they stay in flight together with the kernel's other inputs.
+__device__ __forceinline__ void outcome_load(const PlanArgs &a, int rd, uint64_t (&v)[kCopies]) {
+  const int w = min(lane_id(), kBitWords - 1);
 #pragma unroll
-  for (int c = 0; c < kCopies; ++c)
-    v[c] = lane < kBitWords ? a.ws.bits[(rd * kCopies + c) * kBitWords + lane] : 0;
+  for (int c = 0; c < kCopies; ++c) v[c] = a.ws.bits[(rd * kCopies + c) * kBitWords + w];
+}
+
+// The OR of the copies: word w in lane w, zero past the last word.
+__device__ __forceinline__ uint64_t outcome_or(const uint64_t (&v)[kCopies]) {
   uint64_t bw = 0;
 #pragma unroll
   for (int c = 0; c < kCopies; ++c) bw |= v[c];
-  return bw;
+  return lane_id() < kBitWords ? bw : 0;
 }
 
 // The sequential bisection through round rd's depth-kDepth subtree, from
@@ -553,30 +578,41 @@ __device__ __forceinline__ void walk_bits(uint64_t bw, int rd, BisState &st) {
 __global__ void __launch_bounds__(kWave) k_plan_round(PlanArgs a, int round) {
   __shared__ int32_t s_eorder[kMaxE];
   __shared__ int32_t s_elam[kMaxE];
-  __shared__ uint32_t s_re[kMaxRec];
-  __shared__ int32_t s_rd[kMaxRec];
+  __shared__ uint32_t s_re[kMaxRec + kWave];
+  __shared__ int32_t s_rd[kMaxRec + kWave];
   const int lane = threadIdx.x, b = blockIdx.x;
   const int R = a.R, E = a.E, RS = R * a.NS;
-  // every input is requested up front, so the round waits for memory once:
-  // the state before the previous round and that round's outcome bits, the
-  // per-rank expert orders and the rank orders
+  // every input is requested up front, with no branch between the loads
+  // (indices clamped into range, values masked afterwards), so the round
+  // waits for memory once: the state before the previous round and that
+  // round's outcome bits (round 0 reads the last round's words, which
+  // nothing writes before that round), the per-rank expert orders and the
+  // rank orders
   const int64_t status = a.ws.hdr[3];
   const bool packed = a.ws.hdr[1] < (int64_t(1) << 25);
   BisState st = state_before(a, round > 0 ? round - 1 : 0);
-  const uint64_t bw = round > 0 ? outcome_words(a, round - 1) : 0;
+  uint64_t bv[kCopies];
+  outcome_load(a, round > 0 ? round - 1 : kRounds - 1, bv);
   int ve[kMaxE / kWave], vl[kMaxE / kWave];
 #pragma unroll
   for (int u = 0; u < kMaxE / kWave; ++u) {
-    const int i = u * kWave + lane;
-    ve[u] = i < E ? a.ws.eorder[i] : 0;
-    vl[u] = i < E ? a.ws.elam[i] : 0;
+    if (u * kWave < E) {
+      const int i = min(u * kWave + lane, E - 1);  // stored to LDS only below E
+      ve[u] = a.ws.eorder[i];
+      vl[u] = a.ws.elam[i];
+    }
   }
-  const int rk_r = lane < R ? a.ws.rank_desc[lane] : 0;
-  const int as_r = lane < R ? a.ws.rank_asc[lane] : 0;
-  const int ell_lane = lane < R ? a.ws.ell[lane] : 0;
+  const int lr = min(lane, R - 1);
+  const int rk_v = a.ws.rank_desc[lr], as_v = a.ws.rank_asc[lr], ell_v = a.ws.ell[lr];
+  // the loads above are issued before the status test (which the compiler
+  // would otherwise move ahead of them, waiting for the header first)
+  asm volatile("" ::: "memory");
+  const int rk_r = lane < R ? rk_v : 0;
+  const int as_r = lane < R ? as_v : 0;
+  const int ell_lane = lane < R ? ell_v : 0;
   if (status != 0) return;
   if (round > 0) {  // every workgroup walks the previous round; the first publishes it
-    walk_bits(bw, round - 1, st);
+    walk_bits(outcome_or(bv), round - 1, st);
     if (b == 0 && lane == 0) {
       int64_t *h = a.ws.hdr + 4 + 4 * (round - 1);
       h[0] = st.lo;
@@ -715,7 +751,9 @@ __device__ __forceinline__ int ahead(int key) {
 // then u_i -= q_i.  The shares go to s_q[r * 8 + i] (lanes past 7 write a
 // spare area); afterwards lane r writes source r's row of Q, adding the
 // locality share of the host that is r itself.  s_hosts lists the hosts'
-// ranks, s_q holds kRrLds - kWave ints.
+// ranks, s_q holds kRrLds - kWave ints.  kSmall (the expert's residual
+// demand below 2^19): the same with an fp32 estimate and 24-bit products.
+template <bool kSmall>
 __device__ __forceinline__ void split_lanes8(int lane, int nh, int lamhat_r, int Dr, int loc_r,
                                              int R, int64_t ncol, int32_t *qbase,
                                              const int32_t *s_hosts, int32_t *s_q,
@@ -724,34 +762,70 @@ __device__ __forceinline__ void split_lanes8(int lane, int nh, int lamhat_r, int
   const bool slot = lane < 16 && hidx < nh;
   int ures = __shfl(ures_r, slot ? s_hosts[hidx] : 0);
   ures = slot ? ures : 0;
-  // lh / D of source `lane`
-  const double c_r = lamhat_r > 0 ? static_cast<double>(lamhat_r) / static_cast<double>(Dr) : 0.0;
   const int qstep = lane < 8 ? 8 : 0;
   const int qoff = lane < 8 ? lane : 8 * kMaxR + lane;
   uint64_t act = ballot(lane < R && lamhat_r > 0);
   const int key_lo = 7 - hidx;
-  while (act) {
-    const int r = __ffsll(static_cast<unsigned long long>(act)) - 1;
-    act &= act - 1;
-    const int lh = readlane(lamhat_r, r);
-    const int D = readlane(Dr, r);
-    const double c = readlane_d(c_r, r);
-    const int be = static_cast<int>(c * static_cast<double>(ures));
-    const int re = static_cast<int>(static_cast<uint32_t>(lh) * static_cast<uint32_t>(ures) -
-                                    static_cast<uint32_t>(be) * static_cast<uint32_t>(D));
-    const bool lo = re < 0, hi = re >= D;
-    const int b = lo ? be - 1 : (hi ? be + 1 : be);
-    const int rem = lo ? re + D : (hi ? re - D : re);
-    int sb = b + row_ror<4>(b);
-    sb += row_ror<2>(sb);
-    sb += row_ror<1>(sb);
-    const int left = lh - sb;
-    const int key = rem * 8 + key_lo;
-    const int rk = (ahead<1>(key) + ahead<2>(key)) + (ahead<3>(key) + ahead<4>(key)) +
-                   ((ahead<5>(key) + ahead<6>(key)) + ahead<7>(key));
-    const int qi = b + ((slot && rk < left) ? 1 : 0);
-    ures -= qi;
-    s_q[r * qstep + qoff] = qi;
+  if (kSmall) {
+    // Residual demand below 2^19: c = (lh / D)(1 - 2^-20) rounded to fp32
+    // makes y = fl(c * u) fall strictly below x = lh * u / D and above
+    // x - 1 (relative errors below 2^-20 + 2^-23 on x < 2^19), so trunc(y)
+    // is floor(x) or floor(x) - 1, and the remainder lh * u - trunc(y) * D
+    // lies in [0, 2D): 24-bit products wrapped to 32 bits give it exactly,
+    // and one subtraction with a min gives the floor's remainder
+    const float c_r = lamhat_r > 0 ? static_cast<float>(static_cast<double>(lamhat_r) *
+                                                        (1.0 - 0x1p-20) / static_cast<double>(Dr))
+                                   : 0.0f;
+    const int nD_r = -Dr;
+    while (act) {
+      const int r = __ffsll(static_cast<unsigned long long>(act)) - 1;
+      act &= act - 1;
+      const int lh = readlane(lamhat_r, r);
+      const int nD = readlane(nD_r, r);
+      const float c = __int_as_float(readlane(__float_as_int(c_r), r));
+      const int be = static_cast<int>(c * static_cast<float>(ures));
+      const int re = static_cast<int>(static_cast<uint32_t>(__mul24(be, nD)) +
+                                      __umul24(lh, static_cast<uint32_t>(ures)));
+      const int t = re + nD;  // re - D, in [-D, D)
+      const int rem = static_cast<int>(min(static_cast<uint32_t>(re), static_cast<uint32_t>(t)));
+      const int b = be + 1 + (t >> 31);
+      int sb = b + row_ror<4>(b);
+      sb += row_ror<2>(sb);
+      sb += row_ror<1>(sb);
+      const int left = lh - sb;
+      const int key = rem * 8 + key_lo;
+      const int rk = (ahead<1>(key) + ahead<2>(key)) + (ahead<3>(key) + ahead<4>(key)) +
+                     ((ahead<5>(key) + ahead<6>(key)) + ahead<7>(key));
+      const int qi = b + ((slot && rk < left) ? 1 : 0);
+      ures -= qi;
+      s_q[r * qstep + qoff] = qi;
+    }
+  } else {
+    // lh / D of source `lane`
+    const double c_r = lamhat_r > 0 ? static_cast<double>(lamhat_r) / static_cast<double>(Dr) : 0.0;
+    while (act) {
+      const int r = __ffsll(static_cast<unsigned long long>(act)) - 1;
+      act &= act - 1;
+      const int lh = readlane(lamhat_r, r);
+      const int D = readlane(Dr, r);
+      const double c = readlane_d(c_r, r);
+      const int be = static_cast<int>(c * static_cast<double>(ures));
+      const int re = static_cast<int>(static_cast<uint32_t>(lh) * static_cast<uint32_t>(ures) -
+                                      static_cast<uint32_t>(be) * static_cast<uint32_t>(D));
+      const bool lo = re < 0, hi = re >= D;
+      const int b = lo ? be - 1 : (hi ? be + 1 : be);
+      const int rem = lo ? re + D : (hi ? re - D : re);
+      int sb = b + row_ror<4>(b);
+      sb += row_ror<2>(sb);
+      sb += row_ror<1>(sb);
+      const int left = lh - sb;
+      const int key = rem * 8 + key_lo;
+      const int rk = (ahead<1>(key) + ahead<2>(key)) + (ahead<3>(key) + ahead<4>(key)) +
+                     ((ahead<5>(key) + ahead<6>(key)) + ahead<7>(key));
+      const int qi = b + ((slot && rk < left) ? 1 : 0);
+      ures -= qi;
+      s_q[r * qstep + qoff] = qi;
+    }
   }
   if (lane < R) {
     const bool dem = lamhat_r > 0;
@@ -853,7 +927,12 @@ __device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0,
     if ((rep >> lane) & 1) s_t[1 + popc_below(rep)] = lane;
     __syncthreads();
     if (exact && nh <= 8) {
-      split_lanes8(lane, nh, lamhat_r, Dr, loc_r, R, ncol, a.q + j0, s_t, s_t + kWave, ures_r);
+      if (D0 < (1 << 19))
+        split_lanes8<true>(lane, nh, lamhat_r, Dr, loc_r, R, ncol, a.q + j0, s_t, s_t + kWave,
+                           ures_r);
+      else
+        split_lanes8<false>(lane, nh, lamhat_r, Dr, loc_r, R, ncol, a.q + j0, s_t, s_t + kWave,
+                            ures_r);
       for (int j = total + e; j < ncol; j += E)
         if (lane < R) qrow[j] = 0;
       return;
@@ -896,22 +975,25 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   const int64_t status = a.ws.hdr[3], L = a.ws.hdr[2];
   const int64_t lo0 = a.ws.hdr[0], hi0 = a.ws.hdr[1];
   BisState fin = state_before(a, kRounds - 1);
-  const uint64_t bw = outcome_words(a, kRounds - 1);
+  uint64_t bv[kCopies];
+  outcome_load(a, kRounds - 1, bv);
   const int lam_e = a.ws.lam[e];
-  const int lam_r = kReroute && lane < R ? a.load[static_cast<int64_t>(lane) * E + e] : 0;
+  const int lam_v = kReroute ? a.load[static_cast<int64_t>(min(lane, R - 1)) * E + e] : 0;
+  asm volatile("" ::: "memory");  // the loads above go out before the status test
+  const int lam_r = lane < R ? lam_v : 0;
   if (status != 0) {
     if (e == 0 && lane < 8) a.stats[lane] = lane == 6 ? ULTRAEP_EDATA : (lane == 7 ? L : 0);
     return;
   }
-  walk_bits(bw, kRounds - 1, fin);
+  walk_bits(outcome_or(bv), kRounds - 1, fin);
   int nb = 0;  // transfers of the last feasible probe, read into s_et / s_d
   if (fin.lo < fin.hi) {
     // a bisection longer than the rounds: the remaining probes run here, one
     // after another, the same ones in every workgroup
     __shared__ int32_t s_eorder[kMaxE];
     __shared__ int32_t s_elam[kMaxE];
-    __shared__ uint32_t s_re[kMaxRec];
-    __shared__ int32_t s_rd[kMaxRec];
+    __shared__ uint32_t s_re[kMaxRec + kWave];
+    __shared__ int32_t s_rd[kMaxRec + kWave];
     for (int i = lane; i < E; i += kWave) {
       s_eorder[i] = a.ws.eorder[i];
       s_elam[i] = a.ws.elam[i];
@@ -949,11 +1031,26 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   const int n_probe = fin.probes;
   const int best = fin.best;
   if (best >= 0) {
-    nb = a.ws.res[best];
+    // the count and the node's records are requested together: every slot's
+    // record is read (at most RS), the ones past the count are dropped
     const uint32_t *rec = a.ws.rec + static_cast<int64_t>(best) * 2 * RS;
-    for (int i = lane; i < nb; i += kWave) {
-      s_et[i] = rec[2 * i];
-      s_d[i] = static_cast<int32_t>(rec[2 * i + 1]);
+    uint32_t rv_e[kMaxRec / kWave], rv_d[kMaxRec / kWave];
+#pragma unroll
+    for (int u = 0; u < kMaxRec / kWave; ++u) {
+      if (u * kWave < RS) {
+        const int i = min(u * kWave + lane, RS - 1);
+        rv_e[u] = rec[2 * i];
+        rv_d[u] = rec[2 * i + 1];
+      }
+    }
+    nb = a.ws.res[best];
+#pragma unroll
+    for (int u = 0; u < kMaxRec / kWave; ++u) {
+      const int i = u * kWave + lane;
+      if (u * kWave < RS && i < nb) {
+        s_et[i] = rv_e[u];
+        s_d[i] = static_cast<int32_t>(rv_d[u]);
+      }
     }
   }
   __syncthreads();
@@ -969,27 +1066,46 @@ __global__ void __launch_bounds__(kWave) k_plan_emit(PlanArgs a) {
   before = wave_sum(before);
   shed = wave_sum(shed);
   const int hp_e = e + before;
-  // this expert's replicas: position among them = replicas on lower ranks;
-  // slot on the host = earlier accepted transfers to the same rank
-  int fan = 0;
+  // this expert's replicas: position among them = replicas on lower ranks
+  // (an expert's transfers go to distinct ranks, so a mask of them gives
+  // it); slot on the host = earlier accepted transfers to the same rank,
+  // from a match of equal ranks within 64 records and per-rank counts of
+  // the records before them
+  uint64_t tmask = 0;
   for (int i0 = 0; i0 < nb; i0 += kWave) {
     const int i = i0 + lane;
-    const bool mine = i < nb && static_cast<int>(s_et[i] & 0xFFFFu) == e;
-    const uint64_t mb = ballot(mine);
-    if (mine) {
-      const int t = static_cast<int>(s_et[i] >> 16);
-      int pos = 0, slot = 0;
-      for (int j = 0; j < nb; ++j) {
-        const uint32_t x = s_et[j];
-        pos += static_cast<int>(x & 0xFFFFu) == e && static_cast<int>(x >> 16) < t;
-        slot += j < i && static_cast<int>(x >> 16) == t;
-      }
-      s_ht[1 + pos] = t;
-      s_hu[1 + pos] = s_d[i];
-      a.hr[hp_e + 1 + pos] = t;
-      a.hs[hp_e + 1 + pos] = nm + slot;
+    const uint32_t x = i < nb ? s_et[i] : 0xFFFFFFFFu;  // expert field 0xFFFF: no expert
+    uint64_t mb = ballot(static_cast<int>(x & 0xFFFFu) == e);
+    while (mb) {
+      const int l = __ffsll(static_cast<unsigned long long>(mb)) - 1;
+      mb &= mb - 1;
+      tmask |= uint64_t(1) << readlane(static_cast<int>(x >> 16), l);
     }
-    fan += __popcll(mb);
+  }
+  const int fan = __popcll(tmask);
+  if (fan > 0) {
+    const int tb = bits_for(R);
+    for (int i = lane; i < kMaxR; i += kWave) s_fan[i] = 0;  // records per rank so far
+    __syncthreads();
+    for (int i0 = 0; i0 < nb; i0 += kWave) {
+      const int i = i0 + lane;
+      const bool valid = i < nb;
+      const uint32_t x = valid ? s_et[i] : 0;
+      const int t = static_cast<int>(x >> 16);
+      const uint64_t same = match_any(static_cast<uint32_t>(t), tb, ballot(valid));
+      const int before_t = valid ? s_fan[t] : 0;
+      if (valid && static_cast<int>(x & 0xFFFFu) == e) {
+        const int pos = __popcll(tmask & ((uint64_t(1) << t) - 1));
+        const int slot = before_t + popc_below(same);
+        s_ht[1 + pos] = t;
+        s_hu[1 + pos] = s_d[i];
+        a.hr[hp_e + 1 + pos] = t;
+        a.hs[hp_e + 1 + pos] = nm + slot;
+      }
+      __syncthreads();
+      if (valid && popc_below(same) == 0) s_fan[t] = before_t + __popcll(same);
+      __syncthreads();
+    }
   }
   const int nh = 1 + fan;
   if (lane == 0) {
