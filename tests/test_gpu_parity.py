@@ -105,6 +105,57 @@ def test_plan_large_loads(seed, R, E, NS, base, hot, n_hot):
     check_plan(load, og, op)
 
 
+def _many_transfers_load(seed):
+    """64 ranks, 8 experts each, a seeded set of hot ranks whose every expert
+    is heavy: the plans move 100-144 transfers, so the records of the best
+    probe span two or three waves of 64."""
+    rng = np.random.default_rng(seed)
+    R, E = 64, 512
+    NS = int(rng.choice([2, 3, 4]))
+    u_min = int(rng.choice([1, 8, 64]))
+    nm = E // R
+    load = rng.integers(0, 50, (R, E))
+    for h in rng.choice(R, int(rng.integers(8, 40)), replace=False):
+        load[:, h * nm:(h + 1) * nm] += rng.integers(50, 400, (R, nm))
+    return load.astype(np.int32), R, E, NS, u_min
+
+
+@pytest.mark.parametrize("seed", [13, 15, 28, 31, 45, 52])
+def test_plan_many_transfers(seed):
+    """More than 64 accepted transfers: the round's record copy, the emit's
+    record read, host positions and per-rank slot counts across waves of
+    64 records, relay trees and the packing of the rank with the most
+    outbound replicas, against the oracle."""
+    load, R, E, NS, u_min = _many_transfers_load(seed)
+    g, og = gp.groups(R, E, NS, u_min)
+    op = oracle.plan(load, og)
+    assert op.status == oracle.OK and op.stats[4] > 64
+    gp.assert_plan_equal(gp.gpu_plan(load, g), op)
+    gp.assert_plan_equal(gp.gpu_plan(load, g, split=True), op)
+    check_plan(load, og, op)
+    plan = gp.gpu_plan(load, g)
+    rel = oracle.relay(og, op, 1)
+    src = torch.empty(R * NS, dtype=torch.int32, device=gp.DEV)
+    vol = torch.empty(R, dtype=torch.int32, device=gp.DEV)
+    rst = torch.empty(4, dtype=torch.int64, device=gp.DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=gp.DEV)
+    uep.ultraep_relay_plan(g, plan, 1, src, vol, rst, st)
+    gp.assert_same("slot_src", src.cpu().numpy(), rel.slot_src.reshape(-1))
+    X = op.slot_expert.reshape(R, NS)
+    rank = int(np.argmax([((X >= 0) & (X // (E // R) == r)).sum() for r in range(R)]))
+    rng = np.random.default_rng(seed)
+    W = 1032
+    w_h = rng.integers(0, 1 << 16, (E // R, W), dtype=np.uint16)
+    ostg, odoff, n_out, ost = oracle.pack(w_h, rank, og, op, R * NS)
+    assert ost == 0 and n_out > 0
+    stg = torch.empty((n_out, W), dtype=torch.int16, device=gp.DEV)
+    doff = torch.empty(R + 1, dtype=torch.int64, device=gp.DEV)
+    uep.ultraep_pack_replicas(gp.dev_u16(w_h), W, rank, g, plan, stg, n_out, doff, st)
+    gp.assert_same("staging", gp.host_u16(stg), ostg[:n_out])
+    gp.assert_same("dest_off", doff.cpu().numpy(), odoff)
+    assert int(st.item()) == 0
+
+
 def test_tiny_every_rank():
     c, g, og, tk = _workload(1, 0)
     load, _ = oracle.count(tk, c.E, c.R)
