@@ -31,6 +31,12 @@ constexpr int kSlotsPerWave = kDispatchChunk / kDlWaves;  // 128
 constexpr int kMaxBlocks = 2048;                           // R * S
 
 static_assert(kSlotsPerWave % kWave == 0, "chunk must split into wave steps");
+// CSR columns (E + R * n_slot <= 1024 + 256) and start pointers (E + 1) per
+// thread when a 1024-thread workgroup stages them
+constexpr int kLutIters = 2;
+constexpr int kSumBatch = 16;  // chunk histograms summed per batch of loads
+static_assert(kLutIters * kDlThreads >= 1024 + 256 && kLutIters * kDlThreads >= 1024 + 1,
+              "the lookup tables fit the staging loops");
 constexpr int kSteps = kSlotsPerWave / kWave;  // 64-slot steps per wave
 
 size_t dispatch_ws_bytes(int64_t V, int32_t E, int32_t ncol) {
@@ -99,19 +105,48 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_hist(DlArgs a) {
     return;
   }
   // ---- layout workgroup: block sizes, offsets, entry lookup tables ----
-  int32_t *cnt = lds;  // [R*S]
-  int32_t *tmp = lds + kMaxBlocks;
+  // Every input is requested at once (indices clamped into range, no branch
+  // between the loads) and staged in LDS: the CSR start pointers and, per
+  // CSR column, the host rank, its slot and this rank's share.
+  const int ncol = a.ncol;
+  int32_t *cnt = lds;                  // [R*S]
+  int32_t *tmp = lds + kMaxBlocks;     // [kDlWaves]
+  int32_t *l_hp = tmp + kDlWaves + 1;  // [E + 1]
+  int32_t *l_hr = l_hp + E + 1;        // [ncol]
+  int32_t *l_hs = l_hr + ncol;         // [ncol]
+  int32_t *l_q = l_hs + ncol;          // [ncol]
+  int vhp[kLutIters], vhr[kLutIters], vhs[kLutIters], vq[kLutIters];
+#pragma unroll
+  for (int u = 0; u < kLutIters; ++u) {
+    if (u * kDlThreads <= E) vhp[u] = a.hp[min(u * kDlThreads + tid, E)];
+    if (u * kDlThreads < ncol) {
+      const int j = min(u * kDlThreads + tid, ncol - 1);
+      vhr[u] = a.hr[j];
+      vhs[u] = a.hs[j];
+      vq[u] = a.q[j];
+    }
+  }
   const int nblk = a.R * a.S;
   for (int b = tid; b < nblk; b += kDlThreads) cnt[b] = 0;
+#pragma unroll
+  for (int u = 0; u < kLutIters; ++u) {
+    const int i = u * kDlThreads + tid;
+    if (i <= E) l_hp[i] = vhp[u];
+    if (i < ncol) {
+      l_hr[i] = vhr[u];
+      l_hs[i] = vhs[u];
+      l_q[i] = vq[u];
+    }
+  }
   __syncthreads();
-  const int total = a.hp[E];
-  if (total < E || total > a.ncol) {  // not a plan of this group
+  const int total = l_hp[E];
+  if (total < E || total > ncol) {  // not a plan of this group
     if (tid == 0) report(a.status, ULTRAEP_EDATA);
     return;
   }
   for (int j = tid; j < total; j += kDlThreads) {
-    const int t = a.hr[j], p = a.hs[j];
-    if (t >= 0 && t < a.R && p >= 0 && p < a.S) cnt[t * a.S + p] = a.q[j];
+    const int t = l_hr[j], p = l_hs[j];
+    if (t >= 0 && t < a.R && p >= 0 && p < a.S) cnt[t * a.S + p] = l_q[j];
     else report(a.status, ULTRAEP_EDATA);
   }
   __syncthreads();
@@ -141,11 +176,11 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_hist(DlArgs a) {
   __syncthreads();
   for (int e = tid; e < E; e += kDlThreads) {
     int C = 0;
-    for (int j = a.hp[e]; j < a.hp[e + 1]; ++j) {
-      const int t = a.hr[j], p = a.hs[j];
+    for (int j = l_hp[e]; j < l_hp[e + 1]; ++j) {
+      const int t = l_hr[j], p = l_hs[j];
       const bool ok = t >= 0 && t < a.R && p >= 0 && p < a.S;
       a.ws.ent_base[j] = (ok ? cnt[t * a.S + p] : 0) - C;
-      C += a.q[j];
+      C += l_q[j];
       a.ws.ent_cum[j] = C;
     }
     a.ws.exp_tot[e] = C;
@@ -155,49 +190,83 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_hist(DlArgs a) {
 __global__ void __launch_bounds__(kDlThreads) k_dl_rows(DlArgs a) {
   extern __shared__ int32_t lds[];
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  const int E = a.E;
+  const int E = a.E, ncol = a.ncol;
   const int c = blockIdx.x;
   int32_t *whist = lds;  // [kDlWaves][E]
   int32_t *base = lds + kDlWaves * E;
+  // Every input is requested at once (indices clamped into range, no branch
+  // between the loads), so the workgroup waits for memory once: its slots'
+  // expert ids, the histograms of the chunks before it (of every chunk in
+  // workgroup 0, which checks them against the expected totals) and the
+  // instance lookup tables.
+  const int64_t s0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kSlotsPerWave;
+  int32_t ev[kSteps];
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) ev[s] = a.topk[min(s0 + s * kWave + lane, a.V - 1)];
+  const int e_t = min(tid, E - 1);  // this thread's expert for the sums (tid < E)
+  const int nsum = c == 0 ? static_cast<int>(a.ws.n_chunks) : c;
+  const int32_t *h = a.ws.hist + e_t;
+  int hv[kSumBatch];
+#pragma unroll
+  for (int u = 0; u < kSumBatch; ++u) hv[u] = h[min(u, nsum - 1) * static_cast<int64_t>(E)];
+  const int exp_tot = c == 0 ? a.ws.exp_tot[e_t] : 0;
+  int vhp[kLutIters], vcum[kLutIters], vbase[kLutIters];
+  if (a.stage_lut) {
+#pragma unroll
+    for (int u = 0; u < kLutIters; ++u) {
+      if (u * kDlThreads <= E) vhp[u] = a.hp[min(u * kDlThreads + tid, E)];
+      if (u * kDlThreads < ncol) {
+        const int jj = min(u * kDlThreads + tid, ncol - 1);
+        vcum[u] = a.ws.ent_cum[jj];
+        vbase[u] = a.ws.ent_base[jj];
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s)
+    if (s0 + s * kWave + lane >= a.V) ev[s] = -1;
   // instance lookup tables, staged in LDS when they fit
   const int32_t *l_hp = a.hp, *l_cum = a.ws.ent_cum, *l_base = a.ws.ent_base;
   if (a.stage_lut) {
     int32_t *p = base + E;
-    for (int i = tid; i <= E; i += kDlThreads) p[i] = a.hp[i];
-    for (int i = tid; i < a.ncol; i += kDlThreads) {
-      p[E + 1 + i] = a.ws.ent_cum[i];
-      p[E + 1 + a.ncol + i] = a.ws.ent_base[i];
+#pragma unroll
+    for (int u = 0; u < kLutIters; ++u) {
+      const int ii = u * kDlThreads + tid;
+      if (ii <= E) p[ii] = vhp[u];
+      if (ii < ncol) {
+        p[E + 1 + ii] = vcum[u];
+        p[E + 1 + ncol + ii] = vbase[u];
+      }
     }
     l_hp = p;
     l_cum = p + E + 1;
-    l_base = p + E + 1 + a.ncol;
+    l_base = p + E + 1 + ncol;
   }
-  for (int e = tid; e < E; e += kDlThreads) {
-    // sums over chunk histograms with 8 independent loads in flight
-    const int32_t *h = a.ws.hist + e;
-    const int nsum = c == 0 ? static_cast<int>(a.ws.n_chunks) : c;
+  // base ordinals: sums over the earlier chunks' histograms (further batches
+  // of kSumBatch loads when there are more chunks than one batch)
+  if (tid < E) {
     int s = 0, tot = 0;
-    for (int c0 = 0; c0 < nsum; c0 += 8) {
-      int v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = c0 + u < nsum ? h[(c0 + u) * static_cast<int64_t>(E)] : 0;
+    for (int u = 0; u < kSumBatch; ++u) {
+      const int v = u < nsum ? hv[u] : 0;
+      s += u < c ? v : 0;
+      tot += v;
+    }
+    for (int c0 = kSumBatch; c0 < nsum; c0 += kSumBatch) {
+      int w[kSumBatch];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        s += c0 + u < c ? v[u] : 0;
-        tot += v[u];
+      for (int u = 0; u < kSumBatch; ++u) w[u] = h[min(c0 + u, nsum - 1) * static_cast<int64_t>(E)];
+#pragma unroll
+      for (int u = 0; u < kSumBatch; ++u) {
+        const int v = c0 + u < nsum ? w[u] : 0;
+        s += c0 + u < c ? v : 0;
+        tot += v;
       }
     }
-    base[e] = s;
-    if (c == 0 && tot != a.ws.exp_tot[e]) report(a.status, ULTRAEP_EDATA);
+    base[tid] = s;
+    if (c == 0 && tot != exp_tot) report(a.status, ULTRAEP_EDATA);
   }
   for (int i = tid; i < kDlWaves * E; i += kDlThreads) whist[i] = 0;
-  const int64_t s0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kSlotsPerWave;
-  int32_t ev[kSteps];
-#pragma unroll
-  for (int s = 0; s < kSteps; ++s) {
-    const int64_t i = s0 + s * kWave + lane;
-    ev[s] = i < a.V ? a.topk[i] : -1;
-  }
   __syncthreads();
   int32_t *wh = whist + wave * E;
   // pass 1: per-wave counts
@@ -273,7 +342,8 @@ hipError_t launch_dispatch_layout(const int32_t *topk, int64_t V, int32_t rank,
   a.status = status;
   a.stage_lut = 0;
   const size_t lds_hist = sizeof(int32_t) * kDlWaves * g.E;
-  const size_t lds_lay = sizeof(int32_t) * (kMaxBlocks + kDlWaves + 1);
+  const size_t lds_lay =
+      sizeof(int32_t) * (kMaxBlocks + kDlWaves + 1 + g.E + 1 + 3 * static_cast<size_t>(a.ncol));
   hipLaunchKernelGGL(k_dl_hist, dim3(ws.n_chunks + 1), dim3(kDlThreads),
                      lds_hist > lds_lay ? lds_hist : lds_lay, stream, a);
   hipError_t err = hipGetLastError();
