@@ -732,6 +732,22 @@ __device__ __forceinline__ int ahead(int key) {
   return static_cast<int>(static_cast<uint32_t>(key - row_ror<K>(key)) >> 31);
 }
 
+// Sum over the kH host slots of a row that repeats them with period kH.
+template <int kH>
+__device__ __forceinline__ int host_sum(int b) {
+  int sb = kH == 8 ? b + row_ror<4>(b) : b;
+  sb += row_ror<2>(sb);
+  return sb + row_ror<1>(sb);
+}
+
+// Number of the kH - 1 other host slots whose key is larger.
+template <int kH>
+__device__ __forceinline__ int rank_of(int key) {
+  if (kH == 4) return (ahead<1>(key) + ahead<2>(key)) + ahead<3>(key);
+  return (ahead<1>(key) + ahead<2>(key)) + (ahead<3>(key) + ahead<4>(key)) +
+         ((ahead<5>(key) + ahead<6>(key)) + ahead<7>(key));
+}
+
 // Three to eight hosts, total load below 2^26: host i sits in lane i and in
 // its mirror lane i + 8, so that rotations by 1 .. 7 within the 16 lanes of
 // row 0 bring every other host's value to every host lane with no scalar
@@ -753,19 +769,23 @@ __device__ __forceinline__ int ahead(int key) {
 // locality share of the host that is r itself.  s_hosts lists the hosts'
 // ranks, s_q holds kRrLds - kWave ints.  kSmall (the expert's residual
 // demand below 2^19): the same with an fp32 estimate and 24-bit products.
-template <bool kSmall>
-__device__ __forceinline__ void split_lanes8(int lane, int nh, int lamhat_r, int Dr, int loc_r,
-                                             int R, int64_t ncol, int32_t *qbase,
-                                             const int32_t *s_hosts, int32_t *s_q,
-                                             int ures_r) {
-  const int hidx = lane & 7;
+// kH = 4 (at most four hosts): the slots repeat with period 4 in row 0
+// (lanes i, i + 4, i + 8, i + 12), so three rotations rank the keys
+// rem * 4 + (3 - i) and two sum the floors.
+template <int kH, bool kSmall>
+__device__ __forceinline__ void split_lanes(int lane, int nh, int lamhat_r, int Dr, int loc_r,
+                                            int R, int64_t ncol, int32_t *qbase,
+                                            const int32_t *s_hosts, int32_t *s_q,
+                                            int ures_r) {
+  static_assert(kH == 4 || kH == 8, "host slots mirror with period 4 or 8 in a row");
+  const int hidx = lane & (kH - 1);
   const bool slot = lane < 16 && hidx < nh;
   int ures = __shfl(ures_r, slot ? s_hosts[hidx] : 0);
   ures = slot ? ures : 0;
-  const int qstep = lane < 8 ? 8 : 0;
-  const int qoff = lane < 8 ? lane : 8 * kMaxR + lane;
+  const int qstep = lane < kH ? 8 : 0;
+  const int qoff = lane < kH ? lane : 8 * kMaxR + lane;
   uint64_t act = ballot(lane < R && lamhat_r > 0);
-  const int key_lo = 7 - hidx;
+  const int key_lo = kH - 1 - hidx;
   if (kSmall) {
     // Residual demand below 2^19: c = (lh / D)(1 - 2^-20) rounded to fp32
     // makes y = fl(c * u) fall strictly below x = lh * u / D and above
@@ -789,13 +809,8 @@ __device__ __forceinline__ void split_lanes8(int lane, int nh, int lamhat_r, int
       const int t = re + nD;  // re - D, in [-D, D)
       const int rem = static_cast<int>(min(static_cast<uint32_t>(re), static_cast<uint32_t>(t)));
       const int b = be + 1 + (t >> 31);
-      int sb = b + row_ror<4>(b);
-      sb += row_ror<2>(sb);
-      sb += row_ror<1>(sb);
-      const int left = lh - sb;
-      const int key = rem * 8 + key_lo;
-      const int rk = (ahead<1>(key) + ahead<2>(key)) + (ahead<3>(key) + ahead<4>(key)) +
-                     ((ahead<5>(key) + ahead<6>(key)) + ahead<7>(key));
+      const int left = lh - host_sum<kH>(b);
+      const int rk = rank_of<kH>((rem << (kH == 8 ? 3 : 2)) | key_lo);
       const int qi = b + ((slot && rk < left) ? 1 : 0);
       ures -= qi;
       s_q[r * qstep + qoff] = qi;
@@ -815,13 +830,8 @@ __device__ __forceinline__ void split_lanes8(int lane, int nh, int lamhat_r, int
       const bool lo = re < 0, hi = re >= D;
       const int b = lo ? be - 1 : (hi ? be + 1 : be);
       const int rem = lo ? re + D : (hi ? re - D : re);
-      int sb = b + row_ror<4>(b);
-      sb += row_ror<2>(sb);
-      sb += row_ror<1>(sb);
-      const int left = lh - sb;
-      const int key = rem * 8 + key_lo;
-      const int rk = (ahead<1>(key) + ahead<2>(key)) + (ahead<3>(key) + ahead<4>(key)) +
-                     ((ahead<5>(key) + ahead<6>(key)) + ahead<7>(key));
+      const int left = lh - host_sum<kH>(b);
+      const int rk = rank_of<kH>((rem << (kH == 8 ? 3 : 2)) | key_lo);
       const int qi = b + ((slot && rk < left) ? 1 : 0);
       ures -= qi;
       s_q[r * qstep + qoff] = qi;
@@ -927,12 +937,15 @@ __device__ __forceinline__ void reroute_expert(const PlanArgs &a, int e, int j0,
     if ((rep >> lane) & 1) s_t[1 + popc_below(rep)] = lane;
     __syncthreads();
     if (exact && nh <= 8) {
-      if (D0 < (1 << 19))
-        split_lanes8<true>(lane, nh, lamhat_r, Dr, loc_r, R, ncol, a.q + j0, s_t, s_t + kWave,
-                           ures_r);
-      else
-        split_lanes8<false>(lane, nh, lamhat_r, Dr, loc_r, R, ncol, a.q + j0, s_t, s_t + kWave,
-                            ures_r);
+      int32_t *qb = a.q + j0, *s_q = s_t + kWave;
+      if (D0 < (1 << 19)) {
+        if (nh <= 4)
+          split_lanes<4, true>(lane, nh, lamhat_r, Dr, loc_r, R, ncol, qb, s_t, s_q, ures_r);
+        else
+          split_lanes<8, true>(lane, nh, lamhat_r, Dr, loc_r, R, ncol, qb, s_t, s_q, ures_r);
+      } else {
+        split_lanes<8, false>(lane, nh, lamhat_r, Dr, loc_r, R, ncol, qb, s_t, s_q, ures_r);
+      }
       for (int j = total + e; j < ncol; j += E)
         if (lane < R) qrow[j] = 0;
       return;
