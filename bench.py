@@ -518,6 +518,11 @@ def per_workload(args):
                                         layers), each after an untimed 512 MiB
                                         write that evicts the 256 MB MALL:
                                         median, p10, p90
+      scatter, pack (clean)             the same after an untimed 512 MiB read
+                                        instead: the MALL holds none of the
+                                        kernel's data and no dirty lines, so
+                                        the kernel pays no write-back of
+                                        another kernel's output
     Every layer and microbatch uses the activations and weights of the first
     one's measured rank (the bytes moved do not depend on their values)."""
     import numpy as np
@@ -535,14 +540,19 @@ def per_workload(args):
         return {"median": round(float(np.median(ts)), 2), "p10": round(float(np.percentile(ts, 10)), 2),
                 "p90": round(float(np.percentile(ts, 90)), 2)}
 
-    def cold_us(f, n):
+    scratch_sum = torch.zeros((), dtype=torch.int64, device=dev)
+
+    def cold_us(f, n, clean=False):
         f()
         torch.cuda.synchronize()
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(n)]
         hold_stream()
         for e0, e1 in ev:
-            scratch.zero_()
+            if clean:
+                torch.sum(scratch.view(torch.int64), dim=0, out=scratch_sum)
+            else:
+                scratch.zero_()
             e0.record(stream)
             f()
             e1.record(stream)
@@ -630,6 +640,8 @@ def per_workload(args):
         rec["dispatch_us"] = cold_us(disp_f, n_cold)
         rec["scatter_us"] = cold_us(scat_f, n_cold)
         rec["pack_us"] = cold_us(pack_f, n_cold) if outb[rank] else None
+        rec["scatter_us_clean"] = cold_us(scat_f, n_cold, clean=True)
+        rec["pack_us_clean"] = cold_us(pack_f, n_cold, clean=True) if outb[rank] else None
         torch.cuda.synchronize()
         assert int(st.item()) == 0, int(st.item())
         n_routed = int(boff[-1].item())
@@ -641,6 +653,9 @@ def per_workload(args):
         rec["scatter_GBps"] = round(sb / rec["scatter_us"]["median"] / 1e3, 1)
         rec["pack_bytes"] = pb
         rec["pack_GBps"] = round(pb / rec["pack_us"]["median"] / 1e3, 1) if pb else None
+        rec["scatter_GBps_clean"] = round(sb / rec["scatter_us_clean"]["median"] / 1e3, 1)
+        rec["pack_GBps_clean"] = (round(pb / rec["pack_us_clean"]["median"] / 1e3, 1)
+                                  if pb else None)
         # the CPU baseline on the same inputs, and whether it agrees byte for byte
         base = oracle_baseline(c, tk_all, rank, xw["x_h"], xw["w_h"], cap)
         o = base["outputs"]
@@ -685,6 +700,10 @@ def per_workload(args):
                                "pack_us": round(float(np.median([r["pack_us"]["median"] for r in recs
                                                                  if r["pack_us"]])), 2),
                                "scatter_GBps": med("scatter_GBps"),
+                               "scatter_us_clean": med("scatter_us_clean", "median"),
+                               "pack_us_clean": round(float(np.median(
+                                   [r["pack_us_clean"]["median"] for r in recs
+                                    if r["pack_us_clean"]])), 2),
                                "imbalance_after": med("imbalance_after")},
                     "max": {"count_plan_us": max(r["count_plan_us"] for r in recs),
                             "max_hosts": max(r["max_hosts"] for r in recs)},
