@@ -258,7 +258,7 @@ __device__ __forceinline__ int wave_shl1(int v) {
 // target's slack, so one below u_min makes the probe infeasible, and the
 // target leaves the list, exactly as transfer-by-transfer evaluation finds.
 // The experts are visited in one flat loop (rank by rank, experts by
-// descending load) with scalar loop state and a single exit.
+// descending load) with scalar loop state.
 
 // Loads experts [j0, j0 + 64) of rank r's visiting order into lanes.
 // Lanes past the rank's last expert read that expert and hold zeros: no
