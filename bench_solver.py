@@ -13,9 +13,14 @@ popularity), counts it and plans it on the GPU, then reads the plan back:
   max_hosts                  max_e |H(e)|
   inflight                   share of routed tokens served off their rank
                              (from Q, which applies the locality pass)
-  inflight_no_locality       the same share if every source split its
-                             tokens over the hosts in proportion to their
-                             quotas (no locality pass), sum over experts of
+  inflight_no_locality       the same share without the locality pass (every
+                             source's whole demand split over the hosts by
+                             the sequential largest remainder), from the
+                             oracle's plan in tests/golden/quality_gap.json
+  inflight_no_locality_proportional
+                             the analytic estimate of that share: every
+                             source splits its tokens in proportion to the
+                             quotas, sum over experts of
                              1 - sum_t lambda_{t,e} u_{e,t} / lambda_e, per token
   solve_us                   ultraep_plan device latency: one call of a graph
                              of 20 consecutive calls
@@ -89,7 +94,7 @@ def metrics(load, U, host_ptr, host_rank, Q):
         "sum_hosts": int(nh.sum()),
         "max_hosts": int(nh.max()),
         "inflight": remote / L if L else 0.0,
-        "inflight_no_locality": 1.0 - local_noloc / L if L else 0.0,
+        "inflight_no_locality_proportional": 1.0 - local_noloc / L if L else 0.0,
     }
 
 
@@ -151,16 +156,19 @@ def main():
             assert q["tau_star"] == m["tau_star"], "stored table is of other loads"
             m["tau_min_feasible"] = q["tau_min"]
             m["imbalance_at_tau_min"] = q["imbalance_min"]
+            # the table's plan is the oracle's, which this plan equals
+            assert abs(q["inflight"] - m["inflight"]) < 1e-4, "stored table is of other plans"
+            m["inflight_no_locality"] = q["inflight_no_locality"]
         rows.append(m)
         print(f"# E={E} R={R} n_slot={NS} alpha={alpha}: before {m['imbalance_before']:.2f} "
               f"after {m['imbalance_after']:.3f} replicas {m['replicas']} max|H| {m['max_hosts']} "
-              f"inflight {m['inflight']:.3f}/{m['inflight_no_locality']:.3f} "
+              f"inflight {m['inflight']:.3f}/{m.get('inflight_no_locality', float('nan')):.3f} "
               f"solve {m['solve_us']} us", file=sys.stderr, flush=True)
         del gr, plan, load, tk
     keys = ("imbalance_before", "imbalance_after", "replicas", "sum_hosts", "max_hosts", "inflight",
-            "inflight_no_locality", "solve_us")
+            "inflight_no_locality_proportional", "solve_us")
     if all("imbalance_at_tau_min" in r for r in rows):
-        keys = keys + ("imbalance_at_tau_min",)
+        keys = keys + ("imbalance_at_tau_min", "inflight_no_locality")
     avg = {kk: round(float(np.mean([r[kk] for r in rows])), 4) for kk in keys}
     print(json.dumps({"metric": "solver quality over a grid of synthetic power-law loads (Table 3 metrics)",
                       "settings": len(rows), "tokens_per_rank": args.tokens, "average": avg,

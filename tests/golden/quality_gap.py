@@ -18,6 +18,9 @@ smallest feasible tau.  For every input this script records:
                              from tau_lo0), and the max rank load of that
                              probe's quotas over the mean
   replicas_star / _min       redundant slots the two plans consume
+  inflight, inflight_no_      share of routed tokens served off their rank by
+  locality                   the bisection's plan, with and without the
+                             locality pass of SolveReroute
 Inputs: the five seeded workloads (all 16 microbatches of the drifting
 router, the first 8 prefill layers) and the solver-quality sweep's grid.
 
@@ -60,10 +63,17 @@ def gap_row(load, og):
     mean = L / og.R
     tau_star, lo, hi = (int(v) for v in p.stats[:3])
     U = p.quota.astype(np.int64)
+    # the in-flight token ratio of this plan's reroute, and of the reroute
+    # without the locality pass (every source's whole demand split by the
+    # sequential largest remainder over the quotas), for Table 3's pair
+    q = oracle.plan(load, og, locality=False)
+    assert q.status == oracle.OK
     row = {"tau_lo0": lo, "tau_hi0": hi, "tau_star": tau_star,
            "imbalance_before": round(float(load.sum(0).reshape(og.R, -1).sum(1).max() / mean), 4),
            "imbalance_star": round(float(U.sum(0).max() / mean), 4),
-           "replicas_star": int((p.slot_expert >= 0).sum())}
+           "replicas_star": int((p.slot_expert >= 0).sum()),
+           "inflight": round(oracle.metrics(load, og, p)["inflight_ratio"], 4),
+           "inflight_no_locality": round(oracle.metrics(load, og, q)["inflight_ratio"], 4)}
     if lo >= hi:  # already balanced: the identity plan, no probe
         row.update(tau_min=tau_star, imbalance_min=row["imbalance_star"],
                    replicas_min=row["replicas_star"])
@@ -116,7 +126,8 @@ def main():
            "workloads": wl, "sweep": sw,
            "sweep_average": {k: round(float(np.mean([r[k] for r in sw])), 4)
                              for k in ("imbalance_before", "imbalance_star", "imbalance_min",
-                                       "replicas_star", "replicas_min")}}
+                                       "replicas_star", "replicas_min", "inflight",
+                                       "inflight_no_locality")}}
     with open(OUT, "w") as f:
         json.dump(doc, f, indent=1)
     print(f"wrote {OUT} in {time.time() - t0:.0f} s")

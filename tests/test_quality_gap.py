@@ -3,7 +3,8 @@ greedy-feasible threshold (tests/golden/quality_gap.json, written by
 tests/golden/quality_gap.py with the oracle only): its scan is pinned by the
 hand-derived W1 example (bisection 45, linear scan 38), its rows are
 reproducible, and every row is consistent (tau_lo0 <= tau_min <= tau* <=
-tau_hi0, the scan's probe feasible and the one below it not).  CPU only."""
+tau_hi0, the scan's probe feasible and the one below it not, the in-flight
+ratio with the locality pass at most the one without).  CPU only."""
 import json
 import os
 import sys
@@ -52,6 +53,9 @@ def test_rows_are_consistent(orc):
     for r in rows:
         assert r["tau_lo0"] <= r["tau_min"] <= r["tau_star"] <= max(r["tau_hi0"], r["tau_lo0"])
         assert r["imbalance_min"] <= r["imbalance_before"] + 1e-9
+        # the locality pass serves min(lambda_{t,e}, u_{e,t}) of every source
+        # on its own rank, the most any split can keep there (Sec. 5.2)
+        assert 0.0 <= r["inflight"] <= r["inflight_no_locality"] <= 1.0
 
 
 @pytest.mark.parametrize("idx", [1, 3, 11, 18])

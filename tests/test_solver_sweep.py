@@ -31,7 +31,7 @@ def test_metrics_match_the_oracle_diagnostics(cid):
     # remainder; the sweep reports the proportional share, which it tracks
     q = oracle.plan(load, g, locality=False)
     o2 = oracle.metrics(load, g, q)
-    assert abs(m["inflight_no_locality"] - o2["inflight_ratio"]) < 0.02
+    assert abs(m["inflight_no_locality_proportional"] - o2["inflight_ratio"]) < 0.02
 
 
 def test_metrics_by_hand():
@@ -52,7 +52,7 @@ def test_metrics_by_hand():
     assert m["replicas"] == 1 and m["sum_hosts"] == 3 and m["max_hosts"] == 2
     assert m["inflight"] == pytest.approx(5 / 45)       # rank 0's 5 tokens on rank 1
     # proportional split: local share = 30*25/40 + 10*15/40 + 5*5/5
-    assert m["inflight_no_locality"] == pytest.approx(1 - (18.75 + 3.75 + 5) / 45)
+    assert m["inflight_no_locality_proportional"] == pytest.approx(1 - (18.75 + 3.75 + 5) / 45)
 
 
 @pytest.mark.gpu
