@@ -210,7 +210,9 @@ int ultraep_dispatch(const uint16_t *x, const int32_t *topk, int64_t T,
 
 /* The two halves of ultraep_dispatch, for callers that move the rows
  * themselves or time them apart: the layout (row_of_slot, block_off) and the
- * scatter (send rows; n_routed = block_off + R * S, the routed row count). */
+ * scatter (send rows; n_routed = block_off + R * S, the routed row count,
+ * read on the device: rows n_routed .. T*k - 1 are zero-filled, none when
+ * the count lies outside [0, T*k]). */
 int ultraep_dispatch_layout(const int32_t *topk, int64_t T, int32_t k,
                             int32_t rank, const ultraep_group *g,
                             const ultraep_plan_buf *plan, int32_t *row_of_slot,

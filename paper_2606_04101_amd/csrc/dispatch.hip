@@ -436,8 +436,9 @@ k_scatter(const v4u *__restrict__ x, int64_t T, int32_t k, int32_t nch,
     }
   }
   // rows after the routed ones (masked slots) are zero-filled
+  // a routed count outside [0, V] (not a layout of these slots) fills no row
   const int64_t nr = *n_routed;
-  if (nr < V) {
+  if (nr >= 0 && nr < V) {
     const v4u z = v4u{0u, 0u, 0u, 0u};
     for (int64_t row = nr + gw; row < V; row += nw)
       for (int cc = lane; cc < nch; cc += kWave) send[row * nch + cc] = z;
@@ -476,8 +477,9 @@ k_scatter_wide(const v4u *__restrict__ x, int64_t T, int32_t k, int32_t nch,
       }
     }
   }
+  // a routed count outside [0, V] (not a layout of these slots) fills no row
   const int64_t nr = *n_routed;
-  if (nr < V) {
+  if (nr >= 0 && nr < V) {
     const v4u z = v4u{0u, 0u, 0u, 0u};
     for (int64_t row = nr + gw; row < V; row += nw)
       for (int cc = lane; cc < nch; cc += kWave) send[row * nch + cc] = z;

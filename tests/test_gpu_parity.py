@@ -202,6 +202,42 @@ def test_scatter_row_widths(H):
     gp.check_rank(x, tk[r], None, r, g, og, plan, op, split=True)
 
 
+@pytest.mark.parametrize("H", [1032, 16400])
+def test_scatter_routed_count_out_of_range(H):
+    """The scatter reads the routed row count on the device: with the layout's
+    own count the tail rows are zero-filled; a count below 0 or above T*k
+    (not a layout of these slots) fills no row, and the routed rows are
+    still the oracle's."""
+    R, E, NS, k, T = 4, 16, 2, 2, 700
+    g, og = gp.groups(R, E, NS, 8)
+    rng = np.random.default_rng(H + 1)
+    tk = rng.integers(0, E, (R, T, k)).astype(np.int32)
+    tk[rng.random((R, T, k)) < 0.25] = -1
+    load, _ = oracle.count(tk, E, R)
+    op = oracle.plan(load, og)
+    plan = gp.gpu_plan(load, g)
+    r = 2
+    x = rng.integers(0, 1 << 16, (T, H)).astype(np.uint16)
+    osend, oros, oboff, ost = oracle.dispatch(x, tk[r], r, og, op)
+    assert ost == 0
+    V, nr = T * k, int(oboff[-1])
+    assert 0 < nr < V
+    _, ros, boff, st = gp.gpu_dispatch(x, tk[r], r, g, plan, split=True)
+    assert st == 0 and np.array_equal(ros, oros) and np.array_equal(boff, oboff)
+    ros_d = gp.dev_i32(ros)
+    xd = gp.dev_u16(x)
+    for count in (nr, -5, -(1 << 40), V + 3):
+        send = torch.full((V, H), 0x5A5A, dtype=torch.int16, device=gp.DEV)
+        n = torch.tensor([count], dtype=torch.int64, device=gp.DEV)
+        print(f"scatter H={H} n_routed={count}", flush=True)
+        uep.ultraep_dispatch_scatter(xd, T, k, H, ros_d, n, send)
+        torch.cuda.synchronize()
+        got = gp.host_u16(send)
+        assert np.array_equal(got[:nr], osend[:nr]), f"routed rows differ (n_routed={count})"
+        tail = np.zeros((V - nr, H), np.uint16) if count == nr else np.full((V - nr, H), 0x5A5A, np.uint16)
+        assert np.array_equal(got[nr:], tail), f"tail rows (n_routed={count})"
+
+
 @pytest.mark.parametrize("seed", range(0, 160))
 def test_fuzz_parity(seed):
     case = fuzz.make_case(seed)
