@@ -139,8 +139,12 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_hist(DlArgs a) {
     }
   }
   __syncthreads();
+  // the CSR must start at 0, never decrease and end within the columns,
+  // so every entry index below is inside the tables
   const int total = l_hp[E];
-  if (total < E || total > ncol) {  // not a plan of this group
+  bool bad = l_hp[0] != 0 || total < E || total > ncol;
+  for (int e = tid; e < E; e += kDlThreads) bad |= l_hp[e] > l_hp[e + 1];
+  if (__syncthreads_or(bad)) {  // not a plan of this group
     if (tid == 0) report(a.status, ULTRAEP_EDATA);
     return;
   }
@@ -301,8 +305,10 @@ __global__ void __launch_bounds__(kDlThreads) k_dl_rows(DlArgs a) {
       const int below = popc_below(m);
       const int ord = wh[e] + below;
       if (below == 0) wh[e] += __popcll(m);
-      const int j1 = l_hp[e + 1];
-      int j = l_hp[e];
+      // entry range of e, clamped to the tables (a CSR that is not a plan
+      // of this group cannot send the search outside them)
+      const int j1 = min(max(l_hp[e + 1], 0), a.ncol);
+      int j = min(max(l_hp[e], 0), j1);
       while (j < j1 && l_cum[j] <= ord) ++j;
       if (j < j1) row = l_base[j] + ord;
       // a plan row that does not match these ids can point past the buffer

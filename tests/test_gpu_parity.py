@@ -361,6 +361,30 @@ def test_dispatch_flags_plan_mismatch():
     assert st == uep.ULTRAEP_EDATA
 
 
+@pytest.mark.parametrize("where,value", [(1, 1 << 30), (0, -5), (3, 1), (8, 1 << 20)])
+def test_dispatch_flags_corrupt_host_lists(where, value):
+    """A host list pointer array that is not a CSR of this group (an entry
+    past the columns, a negative start, a decreasing pair, a total past the
+    columns) raises ULTRAEP_EDATA; no row points outside send and no tail
+    row is filled from the unwritten block offsets."""
+    R, E, NS, k, T = 4, 8, 1, 2, 300
+    g, og = gp.groups(R, E, NS, 1)
+    rng = np.random.default_rng(where)
+    tk = rng.integers(0, E, (R, T, k)).astype(np.int32)
+    load, _ = oracle.count(tk, E, R)
+    plan = gp.gpu_plan(load, g)
+    hp = plan.host_ptr.cpu().numpy()
+    hp[where] = value
+    plan.host_ptr.copy_(torch.from_numpy(hp))
+    x = rng.integers(0, 1 << 16, (T, 16)).astype(np.uint16)
+    print(f"corrupt host_ptr[{where}] = {value}", flush=True)
+    for split in (False, True):
+        send, ros, boff, st = gp.gpu_dispatch(x, tk[0], 0, g, plan, split=split)
+        assert st == uep.ULTRAEP_EDATA
+        assert ((ros >= -1) & (ros < T * k)).all()
+        assert (boff == -9).all()
+
+
 def test_pack_flags_small_capacity():
     g, og = gp.groups(4, 8, 1, 1)
     load = np.zeros((4, 8), np.int32)
