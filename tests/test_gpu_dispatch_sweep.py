@@ -5,7 +5,9 @@ expert popularity, a quarter of the slots masked, or ids with repeats), from
 0 to 2500 tokens per rank and top-1 to top-8.  The counts, every plan buffer,
 and for two ranks the dispatch (send, row_of_slot, block_off, through both
 the one-call and the split entry points) and the packing (staging, dest_off)
-are compared with the oracle byte for byte.  Needs an MI355X."""
+are compared with the oracle byte for byte; a second sweep covers the
+relay trees, the relay packing, the combine gather and the gradient
+reduction.  Needs an MI355X."""
 import numpy as np
 import pytest
 import torch
@@ -84,3 +86,43 @@ def test_dispatch_sweep(block):
             raise AssertionError(f"{where}: {ex}") from None
         checked += 1
     assert checked > 200
+
+
+@pytest.mark.parametrize("block", range(2))
+def test_extension_sweep(block):
+    """The adjacent steps on the same routings: relay trees at thresholds 0
+    and 2 and the relay packing of two ranks, the combine gather of one
+    rank's dispatched rows with softmax gates, and the gradient reduction of
+    two ranks, against the oracle."""
+    from test_gpu_combine_reduce import bf16_normals, check_combine, check_reduce, softmax_gates
+    from test_gpu_relay import check as check_relay
+    from test_gpu_relay import check_pack_relay
+    checked = 0
+    for seed in range(1000 + block * 150, 1000 + (block + 1) * 150):
+        rng, tk, R, E, NS, k, T, u_min, H, W = sweep_routing(seed)
+        where = f"seed {seed} (R={R} E={E} n_slot={NS} k={k} T={T} u_min={u_min} H={H} W={W})"
+        g, og = gp.groups(R, E, NS, u_min)
+        try:
+            load, _ = oracle.count(tk, E, R)
+            op = oracle.plan(load, og)
+            if op.status != oracle.OK:
+                continue
+            plan = gp.gpu_plan(load, g)
+            gp.assert_plan_equal(plan, op)
+            X = op.slot_expert.reshape(R, max(NS, 0))
+            outb = [int(((X >= 0) & (X // (E // R) == r)).sum()) for r in range(R)]
+            ranks = sorted({int(np.argmax(outb)), int(rng.integers(0, R))})
+            for threshold in (0, 2):
+                rel = check_relay(g, og, plan, op, threshold)
+                check_pack_relay(g, og, plan, op.slot_expert, rel, W, seed, ranks=ranks)
+            r = ranks[-1]
+            if T > 0:
+                send, ros, _, st = gp.gpu_dispatch(bf16_normals(rng, (T, H)), tk[r], r, g, plan)
+                assert st == 0
+                check_combine(send, softmax_gates(rng, T, k), ros)
+            for r in ranks:
+                check_reduce(g, og, plan, op.slot_expert, r, 4 * int(rng.integers(1, 200)), rng)
+        except AssertionError as ex:
+            raise AssertionError(f"{where}: {ex}") from None
+        checked += 1
+    assert checked > 120
