@@ -22,6 +22,8 @@
  *     owns and allocates every buffer; the library never allocates, never
  *     frees, never synchronises the host, keeps no state between calls and
  *     issues no memset, so every call can be captured into a HIP graph.
+ *     (ultraep_plan_noalloc takes its workspace from a fixed array in the
+ *     library's device memory instead of a caller buffer; see there.)
  *   - Work is enqueued on `stream` in order; results are ready when the
  *     stream reaches that point.  Calls on different streams must use
  *     distinct output and workspace buffers.
