@@ -56,6 +56,24 @@ def hold_stream(ms=40.0):
     torch.cuda._sleep(int(ms * 1e-3 * 2.4e9))
 
 
+def outbound_fan(X, n_main, rank):
+    """Copies of each of `rank`'s main experts in the replica placement X
+    ([R][n_slot] int32, -1 = empty): the fan-out its packing serves."""
+    import numpy as np
+    X = np.asarray(X)
+    return np.bincount(X[(X >= 0) & (X // n_main == rank)] - rank * n_main, minlength=n_main)
+
+
+def algorithmic_bytes(T, H, k, n_routed, W, fan):
+    """Bytes the two HBM-bound launches of a step must move at least:
+    the scatter reads every token row once, writes every routed row once and
+    reads row_of_slot (int32 per slot); the packing reads each replicated
+    blob (W bf16 elements) once and writes it once per copy."""
+    scatter = 2 * T * H + 2 * n_routed * H + 4 * T * k
+    pack = int(sum(2 * W * (1 + int(f)) for f in fan if f > 0))
+    return scatter, pack
+
+
 def kernel_source_digest(files):
     h = hashlib.sha256()
     for f in files:
@@ -122,8 +140,7 @@ def main():
     X = plan.slot_expert.cpu().numpy().reshape(c.R, c.n_slot)
     n_out_r = [int(((X >= 0) & (X // c.n_main == r)).sum()) for r in range(c.R)]
     rank = int(np.argmax(n_out_r))  # ties -> smallest rank
-    fan = np.bincount(X[(X >= 0) & (X // c.n_main == rank)] - rank * c.n_main,
-                      minlength=c.n_main)
+    fan = outbound_fan(X, c.n_main, rank)
     x_h = gen.activations(c, 0, rank)
     w_h = gen.weights(c, rank)
     x = torch.from_numpy(x_h.view(np.int16)).to(dev)
@@ -302,9 +319,7 @@ def main():
     del a, b
 
     # ---------------- algorithmic bytes per launch
-    scatter_bytes = 2 * T * H + 2 * n_routed * H + 4 * V
-    W_bytes = 2 * W
-    pack_bytes = int(sum(W_bytes * (1 + f) for f in fan if f > 0))
+    scatter_bytes, pack_bytes = algorithmic_bytes(T, H, k, n_routed, W, fan)
     kern = {
         "dispatch_scatter": (scatter_bytes, per_call_us["dispatch_scatter"],
                              ["dispatch.hip", "common.hpp"]),
@@ -342,7 +357,7 @@ def main():
             "tokens_per_rank": T,
             "routed_rows": n_routed,
             "replicas_shipped": int(n_out_r[rank]),
-            "expert_blob_bytes": W_bytes,
+            "expert_blob_bytes": 2 * W,
             "timed": ("HIP graph replays of count, replicate, reroute + pack, "
                       "dispatch layout, scatter"),
             "steps_per_graph": G,
@@ -645,10 +660,7 @@ def per_workload(args):
         torch.cuda.synchronize()
         assert int(st.item()) == 0, int(st.item())
         n_routed = int(boff[-1].item())
-        sb = 2 * T * H + 2 * n_routed * H + 4 * V
-        fan = np.bincount(X[(X >= 0) & (X // c.n_main == rank)] - rank * c.n_main,
-                          minlength=c.n_main)
-        pb = int(sum(2 * W * (1 + f) for f in fan if f > 0))
+        sb, pb = algorithmic_bytes(T, H, k, n_routed, W, outbound_fan(X, c.n_main, rank))
         rec["scatter_bytes"] = sb
         rec["scatter_GBps"] = round(sb / rec["scatter_us"]["median"] / 1e3, 1)
         rec["pack_bytes"] = pb
