@@ -141,3 +141,23 @@ def test_invalid_arguments_return_einval_without_launch():
 def test_strerror():
     assert uep.ultraep_strerror(0) == "ok"
     assert "capacity" in uep.ultraep_strerror(uep.ULTRAEP_ENOSPC)
+
+
+def test_header_compiles_as_c_and_links():
+    """include/ultraep.h is a C header: a plain C11 caller of every path entry
+    point (tests/native/abi_consumer.c) compiles with gcc -Wall -Wextra
+    -Werror and links against the library."""
+    import shutil
+    import subprocess
+    import tempfile
+    if not shutil.which("gcc") or not os.path.exists("/opt/rocm/include/hip/hip_runtime_api.h"):
+        pytest.skip("gcc or the HIP headers are not installed")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    with tempfile.TemporaryDirectory() as d:
+        r = subprocess.run(
+            ["gcc", "-std=c11", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+             "-I", os.path.join(root, "include"), "-I", "/opt/rocm/include",
+             os.path.join(root, "tests", "native", "abi_consumer.c"),
+             "-L", os.path.dirname(uep.LIB_PATH), "-lultraep", "-L", "/opt/rocm/lib", "-lamdhip64",
+             "-o", os.path.join(d, "abi_consumer")], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
