@@ -161,3 +161,10 @@ def test_header_compiles_as_c_and_links():
              "-L", os.path.dirname(uep.LIB_PATH), "-lultraep", "-L", "/opt/rocm/lib", "-lamdhip64",
              "-o", os.path.join(d, "abi_consumer")], capture_output=True, text=True)
         assert r.returncode == 0, r.stderr
+
+
+def test_binding_has_every_entry_point_by_name():
+    """The Python binding names each function after the C entry point it
+    calls: every symbol the header declares has a same-named function."""
+    missing = [n for n in declared_symbols() if not callable(getattr(uep, n, None))]
+    assert not missing, missing
