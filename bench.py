@@ -106,6 +106,8 @@ def main():
     ap.add_argument("--workloads", action="store_true",
                     help="instead of the step: count, plan, dispatch and pack of every "
                          "workload, with the oracle beside them (one JSON line each)")
+    ap.add_argument("--only", type=int, action="append", default=None,
+                    help="with --workloads: this workload id only (repeatable)")
     args = ap.parse_args()
     if args.workloads:
         return per_workload(args)
@@ -686,6 +688,8 @@ def per_workload(args):
         return rec, (tk_r, load, plan, rank)
 
     for cid in sorted(gen.WORKLOADS):
+        if args.only and cid not in args.only:
+            continue
         c = gen.config(cid)
         g = uep.Group(c.R, c.E, c.n_slot, c.u_min, c.beta_num, c.beta_den)
         shape = {"R": c.R, "E": c.E, "n_slot": c.n_slot, "k": c.k, "T": c.T, "H": c.H, "F": c.F}
